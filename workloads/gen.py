@@ -1,0 +1,142 @@
+"""Seeded generators for every synthetic input of the verify path.
+
+All generators use numpy's counter-based Philox bit generator, so a given
+(seed, shape) always yields the same array on any machine.  Floating-point
+inputs are drawn in fp32 and stored as bf16 bit patterns (uint16), rounded to
+nearest-even, which is the activation/logit dtype of the served model.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+
+def _rng(seed: int) -> np.random.Generator:
+    return np.random.Generator(np.random.Philox(int(seed)))
+
+
+def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round-to-nearest-even; NaN -> 0x7FC0."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
+    nan = np.isnan(x)
+    if nan.any():
+        r[nan] = 0x7FC0
+    return r
+
+
+def f32_from_bf16_bits(b: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> fp32 (exact)."""
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32)
+
+
+def _outlier_columns(K: int, frac: float, seed: int) -> np.ndarray:
+    n_out = int(round(frac * K))
+    perm = _rng(seed + 0x5EED).permutation(K)
+    return np.sort(perm[:n_out])
+
+
+def linear_activations(M: int, K: int, seed: int, outlier_frac: float = 0.0,
+                       outlier_scale: float = 1.0) -> np.ndarray:
+    """Activations X ~ N(0,1) [M,K] with a fixed set of outlier channels.
+
+    The outlier channels are the first round(outlier_frac*K) indices of a
+    seeded permutation of the K channels; those columns are multiplied by
+    outlier_scale (the per-channel outliers typical of LLM activations).
+    Returns bf16 bits [M,K].
+    """
+    x = _rng(seed).standard_normal((M, K), dtype=np.float32)
+    if outlier_frac > 0.0:
+        cols = _outlier_columns(K, outlier_frac, seed)
+        x[:, cols] *= np.float32(outlier_scale)
+    return bf16_bits_from_f32(x)
+
+
+def linear_weights(N: int, K: int, seed: int, std: float = 0.02) -> np.ndarray:
+    """Weights W ~ N(0, std^2) in nn.Linear layout [N,K] (row = output channel)."""
+    w = _rng(seed).standard_normal((N, K), dtype=np.float32)
+    w *= np.float32(std)
+    return bf16_bits_from_f32(w)
+
+
+def student_t_activations(M: int, K: int, seed: int, df: float = 3.0) -> np.ndarray:
+    """Heavy-tailed activations ~ Student-t(df) [M,K] as bf16 bits."""
+    x = _rng(seed).standard_t(df, size=(M, K)).astype(np.float32)
+    return bf16_bits_from_f32(x)
+
+
+def gated_ffn_input(M: int, inter: int, seed: int, std: float = 1.0) -> np.ndarray:
+    """Fused gate|up projection output [M, 2*inter] as bf16 bits.
+
+    Columns [0, inter) are the gate, [inter, 2*inter) the up projection.
+    """
+    g = _rng(seed).standard_normal((M, 2 * inter), dtype=np.float32)
+    g *= np.float32(std)
+    return bf16_bits_from_f32(g)
+
+
+def accept_logits(B: int, k: int, V: int, seed: int, c: float,
+                  scale: float = 3.0, rank: int = 8):
+    """Target and draft logits with a shared low-rank component.
+
+    S = (A @ Bm) / sqrt(rank), A ~ N(0,1) [B,k+1,rank], Bm ~ N(0,1) [rank,V].
+    z_t = scale*(c*S + sqrt(1-c^2)*E_t)             [B,k+1,V]
+    z_d = scale*(c*S[:, :k] + sqrt(1-c^2)*E_d)      [B,k,V]
+    so each position has marginal N(0, scale^2) logits and the draft/target
+    logits at a position are correlated with coefficient c^2.
+    Returns (z_t bits, z_d bits) as bf16 uint16 arrays.
+    """
+    if not (0.0 <= c <= 1.0):
+        raise ValueError("c must lie in [0, 1]")
+    g = _rng(seed)
+    a = g.standard_normal((B, k + 1, rank), dtype=np.float32)
+    bm = g.standard_normal((rank, V), dtype=np.float32)
+    s = (a.reshape(-1, rank) @ bm).reshape(B, k + 1, V)
+    s *= np.float32(1.0 / math.sqrt(rank))
+    cc = np.float32(c)
+    nn = np.float32(math.sqrt(max(0.0, 1.0 - c * c)))
+    sc = np.float32(scale)
+    zt = g.standard_normal((B, k + 1, V), dtype=np.float32)
+    zt *= nn
+    zt += cc * s
+    zt *= sc
+    zt_bits = bf16_bits_from_f32(zt)
+    del zt
+    zd = g.standard_normal((B, k, V), dtype=np.float32)
+    zd *= nn
+    zd += cc * s[:, :k]
+    zd *= sc
+    zd_bits = bf16_bits_from_f32(zd)
+    return zt_bits, zd_bits
+
+
+def draft_tokens_greedy(zd_bits: np.ndarray) -> np.ndarray:
+    """Argmax drafting (a greedy chain): x_i = argmax_v z_d[b,i,v], lowest index on ties."""
+    zd = f32_from_bf16_bits(zd_bits)
+    return np.argmax(zd, axis=-1).astype(np.int32)
+
+
+def draft_tokens_sampled(zd_bits: np.ndarray, temperature: float, seed: int = 8) -> np.ndarray:
+    """Drafts drawn from softmax(z_d / T) with the Gumbel-max construction.
+
+    x_i = argmax_v (z_d[b,i,v]/T + G_v) with G_v iid standard Gumbel; this
+    draws x_i from the draft's tempered distribution without normalising it.
+    """
+    if temperature <= 0:
+        return draft_tokens_greedy(zd_bits)
+    zd = f32_from_bf16_bits(zd_bits).astype(np.float64) / float(temperature)
+    u = _rng(seed).random(zd.shape)
+    # Gumbel(0,1) = -log(-log U); U=0 has probability ~2^-53 and is nudged.
+    u = np.clip(u, np.finfo(np.float64).tiny, 1.0)
+    zd += -np.log(-np.log(u))
+    return np.argmax(zd, axis=-1).astype(np.int32)
+
+
+def philox_uniforms(shape, seed: int = 7) -> np.ndarray:
+    """Uniforms in [0,1) as fp32 from Philox(seed)."""
+    return _rng(seed).random(shape, dtype=np.float32)
