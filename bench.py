@@ -1,0 +1,302 @@
+"""Bench of the FP8 speculative-verify hot path on one MI355X.
+
+One step = one verify pass of the whole hot path for a serving batch of
+B=64 sequences with k=4 drafted tokens (M = 320 rows):
+  quantize(x_qkv) -> QKV GEMM 4096->6144
+  quantize(x_o)   -> O GEMM 4096->4096
+  quantize(x_mlp) -> gate|up GEMM 4096->28672
+  SiLU-gated quantize of the gate|up output -> down GEMM 14336->4096 (bf16 out)
+  stochastic acceptance (T=0.7) over target/draft logits [64,5|4,128256]
+Weights are quantized once per channel before timing (offline PTQ).  Inputs
+are seeded synthetic tensors resident in HBM; several copies of the weights
+and logits are rotated so that consecutive steps do not hit the 256 MB
+Infinity Cache with the previous step's bytes.
+
+Prints ONE JSON line.  `value` is the verify-step FP8 GEMM throughput over
+the whole step (GEMM FLOPs / step time, quantize and acceptance included);
+the per-part figures (GEMM-only TFLOP/s, acceptance GB/s, verified tokens/s)
+are under "components".
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "verify-step FP8 GEMM TFLOP/s (% MFMA peak); accept GB/s; verified tokens/s"
+PEAK_FP8_TFLOPS = 5000.0     # MI355X dense FP8 MFMA (published)
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E (published)
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def build_inputs(torch, p, wl, copies):
+    cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
+    M = cfg3["M"]
+    dev = "cuda"
+
+    def bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    acts = {}
+    for name, N, K in cfg3["linears"]:
+        if name == "down":
+            continue
+        acts[name] = bf16(wl.linear_activations(M, K, cfg3["seed"] + len(acts), cfg3["act_outlier_frac"],
+                                                cfg3["act_outlier_scale"]))
+    weights = []
+    for c in range(copies):
+        ws = {}
+        for i, (name, N, K) in enumerate(cfg3["linears"]):
+            wb = bf16(wl.linear_weights(N, K, cfg3["seed"] + 17 + 101 * i + 7919 * c, cfg3["w_std"]))
+            q, s = p.quantize(wb)                           # offline per-channel PTQ
+            ws[name] = (q, s.clone())
+            del wb
+        weights.append(ws)
+        log(f"weights copy {c} ready")
+    B, k, V, T = cfg4["B"], cfg4["k"], cfg4["V"], cfg4["temperature"]
+    logits = []
+    for c in range(copies):
+        zt, zd = wl.accept_logits(B, k, V, cfg4["seed"] + 1000 * c, wl.C4_CORRELATION, scale=cfg4["logit_std"],
+                                  rank=cfg4["rank"])
+        x = wl.draft_tokens_sampled(zd, T, seed=cfg4["draft_seed"] + 1000 * c)
+        u = wl.philox_uniforms((B, k + 1), seed=cfg4["uniform_seed"] + 1000 * c)
+        logits.append((bf16(zt), bf16(zd), torch.from_numpy(x).to(dev), torch.from_numpy(u).to(dev)))
+        log(f"logits copy {c} ready")
+    return acts, weights, logits
+
+
+class Step:
+    """Preallocated buffers and the launch sequence of one verify step."""
+
+    def __init__(self, torch, p, wl, acts):
+        cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
+        self.torch, self.p = torch, p
+        M = cfg3["M"]
+        dev = "cuda"
+        self.acts = acts
+        self.lin = {name: (N, K) for name, N, K in cfg3["linears"]}
+        self.q = {n: torch.empty((M, K), dtype=torch.uint8, device=dev) for n, (N, K) in self.lin.items()}
+        self.s = {n: torch.empty((M,), dtype=torch.float32, device=dev) for n in self.lin}
+        self.y = {n: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for n, (N, K) in self.lin.items()}
+        ws = max(p.gemm_workspace_bytes(M, N, K) for N, K in self.lin.values())
+        self.gws = torch.empty((max(ws, 16),), dtype=torch.uint8, device=dev)
+        B, k, V = cfg4["B"], cfg4["k"], cfg4["V"]
+        self.T = cfg4["temperature"]
+        self.aws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device=dev)
+        self.out = torch.empty((B, k + 1), dtype=torch.int32, device=dev)
+        self.num = torch.empty((B,), dtype=torch.int32, device=dev)
+
+    def run(self, weights, logits, ev=None):
+        p = self.p
+        for name in ("qkv", "o", "gate_up"):
+            p.quantize(self.acts[name], out=self.q[name], scales=self.s[name])
+            if ev is not None and name == "gate_up":
+                ev["gu"][0].record()
+            w, sw = weights[name]
+            p.gemm(self.q[name], self.s[name], w, sw, out=self.y[name], workspace=self.gws)
+            if ev is not None and name == "gate_up":
+                ev["gu"][1].record()
+        p.quantize(self.y["gate_up"], silu_mul=True, out=self.q["down"], scales=self.s["down"])
+        w, sw = weights["down"]
+        p.gemm(self.q["down"], self.s["down"], w, sw, out=self.y["down"], workspace=self.gws)
+        zt, zd, x, u = logits
+        if ev is not None:
+            ev["acc"][0].record()
+        p.verify_accept(zt, zd, x, u, self.T, workspace=self.aws, out_tokens=self.out, num_accepted=self.num)
+        if ev is not None:
+            ev["acc"][1].record()
+
+
+def time_parts(torch, step, weights, logits, reps):
+    """Per-part event timing (quantize+GEMM per linear, accept), median over reps."""
+    p = step.p
+    names = ["qkv", "o", "gate_up", "down", "accept"]
+    ts = {n: [] for n in names}
+    for r in range(reps):
+        w = weights[r % len(weights)]
+        lg = logits[r % len(logits)]
+        for n in names:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            if n == "accept":
+                zt, zd, x, u = lg
+                p.verify_accept(zt, zd, x, u, step.T, workspace=step.aws, out_tokens=step.out,
+                                num_accepted=step.num)
+            elif n == "down":
+                p.gemm(step.q["down"], step.s["down"], *w["down"], out=step.y["down"], workspace=step.gws)
+            else:
+                p.gemm(step.q[n], step.s[n], *w[n], out=step.y[n], workspace=step.gws)
+            e1.record()
+            ts[n].append((e0, e1))
+    torch.cuda.synchronize()
+    return {n: float(np.median([a.elapsed_time(b) for a, b in v])) * 1e3 for n, v in ts.items()}
+
+
+def cpu_baseline(wl):
+    """The oracle on a bounded sample of the same workload, on the host cores."""
+    from oracle import accept as oa, gemm as og, quantize as oq
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
+    rows, nfrac, bseq = 16, 8, 8
+    M = cfg3["M"]
+    # untimed: sampled activations, weights for every nfrac-th output channel, oracle-quantized
+    xs = {}
+    for i, (name, N, K) in enumerate(cfg3["linears"]):
+        if name != "down":
+            xs[name] = wl.linear_activations(M, K, cfg3["seed"] + i, cfg3["act_outlier_frac"],
+                                             cfg3["act_outlier_scale"])[:rows]
+    wq = {}
+    for i, (name, N, K) in enumerate(cfg3["linears"]):
+        wb = wl.linear_weights(N, K, cfg3["seed"] + 17 + 101 * i, cfg3["w_std"])[::nfrac]
+        wq[name] = oq.quantize_rows(wb)
+    B, k, V, T = cfg4["B"], cfg4["k"], cfg4["V"], cfg4["temperature"]
+    zt, zd = wl.accept_logits(B, k, V, cfg4["seed"], wl.C4_CORRELATION, scale=cfg4["logit_std"], rank=cfg4["rank"])
+    x = wl.draft_tokens_sampled(zd, T, seed=cfg4["draft_seed"])
+    u = wl.philox_uniforms((B, k + 1), seed=cfg4["uniform_seed"])
+    flops = 0.0
+    t0 = time.perf_counter()
+    gu = None
+    for name, N, K in cfg3["linears"]:
+        if name == "down":
+            inter = wq["gate_up"][0].shape[0] // 2
+            a, sa, _ = oq.quantize_silu_mul_rows(gu[:, :2 * inter])
+        else:
+            a, sa = oq.quantize_rows(xs[name])
+        w, sw = wq[name]
+        y = og.gemm(a, sa, w[:, :a.shape[1]], sw)
+        flops += 2.0 * a.shape[0] * w.shape[0] * a.shape[1]
+        if name == "gate_up":
+            gu = wl.bf16_bits_from_f32(y.astype(np.float32))
+    oa.accept_stochastic(zt[:bseq], zd[:bseq], x[:bseq], u[:bseq], T)
+    dt = time.perf_counter() - t0
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{rows} of {M} rows x every {nfrac}th output channel of the 4 layer linears "
+                      f"(quantize + exact fp64 GEMM + SiLU-gated re-quantize) and stochastic acceptance of "
+                      f"{bseq} of {B} sequences at V={V}; {dt:.2f} s"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--copies", type=int, default=3, help="rotated copies of weights and logits")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}): the verify path runs on one "
+              f"MI355X; a sharded version is a design note, not a measured configuration.", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2606_18502_amd as p
+    import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    p.load_library()
+    torch.cuda.set_device(0)
+    acts, weights, logits = build_inputs(torch, p, wl, args.copies)
+    step = Step(torch, p, wl, acts)
+    cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
+    M = cfg3["M"]
+    gemm_flops = sum(2.0 * M * N * K for _, N, K in cfg3["linears"])
+
+    for i in range(args.warmup):
+        step.run(weights[i % args.copies], logits[i % args.copies])
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    ev = {"gu": [], "acc": []}
+    evs = []
+    for i in range(args.steps):
+        e = {"gu": (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)),
+             "acc": (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))}
+        evs.append(e)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record()
+    for i in range(args.steps):
+        step.run(weights[i % args.copies], logits[i % args.copies], ev=evs[i])
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / args.steps
+    gu_us = float(np.mean([e["gu"][0].elapsed_time(e["gu"][1]) for e in evs])) * 1e3
+    acc_us = float(np.mean([e["acc"][0].elapsed_time(e["acc"][1]) for e in evs])) * 1e3
+    num = step.num.cpu().numpy()
+    tokens = float(np.sum(num + 1))
+    log(f"step {ms_step * 1e3:.1f} us; gate_up gemm {gu_us:.1f} us; accept {acc_us:.1f} us")
+
+    parts = time_parts(torch, step, weights, logits, reps=20)
+    gemm_us = parts["qkv"] + parts["o"] + parts["gate_up"] + parts["down"]
+
+    B, k, V = cfg4["B"], cfg4["k"], cfg4["V"]
+    acc_bytes = 2.0 * B * (2 * k + 1) * V                       # target + draft logits read once
+    N_gu, K_gu = dict((n, (N, K)) for n, N, K in cfg3["linears"])["gate_up"]
+    gu_bytes = M * K_gu + N_gu * K_gu + 4 * (M + N_gu) + 2 * M * N_gu
+    gu_flops = 2.0 * M * N_gu * K_gu
+
+    res = {
+        "metric": METRIC,
+        "value": round(gemm_flops / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp8e4m3 (fp32 accumulate)",
+        "data": "synthetic (seeded; Llama-3.1-8B-shaped weights N(0,0.02), activations N(0,1) with 0.5% x30 "
+                "outlier channels, low-rank-correlated logits)",
+        "config": {"workload": "verify step B=64 k=4 (M=320): QKV 4096->6144, O 4096->4096, gate|up "
+                               "4096->28672, SiLU-gated down 14336->4096 (bf16 out), stochastic acceptance "
+                               "T=0.7 over V=128256", "B": B, "k": k, "M": M, "V": V, "copies": args.copies},
+        "components": {
+            "gemm_only_tflops": round(gemm_flops / (gemm_us * 1e-6) / 1e12, 1),
+            "gemm_only_pct_mfma_peak": round(100 * gemm_flops / (gemm_us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 1),
+            "gemm_us": {n: round(parts[n], 1) for n in ("qkv", "o", "gate_up", "down")},
+            "accept_us": round(acc_us, 1),
+            "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
+            "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),
+            "verified_tokens_per_step": tokens,
+            "verified_tokens_per_s_accept": round(tokens / (acc_us * 1e-6), 0),
+            "verified_tokens_per_s_step": round(tokens / (ms_step * 1e-3), 0),
+        },
+        "roofline": {
+            "kernel": "gate|up FP8 GEMM (M=320, N=28672, K=4096)",
+            "bound": "hbm",
+            "achieved": round(gu_bytes / (gu_us * 1e-6) / 1e9, 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(gu_bytes / (gu_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 3),
+            "traffic": None,
+            "algorithmic_bytes": gu_bytes,
+            "avg_launch_us": round(gu_us, 2),
+            "mfma_frac": round(gu_flops / (gu_us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 3),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        res["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,183 @@
+/*
+ * spec_fp8.h -- C ABI of libspecfp8.so, the FP8 speculative-decoding verify
+ * path for AMD Instinct MI355X (gfx950).
+ *
+ * The verify step of speculative decoding (paper section 3.1, EAGLE): a draft
+ * model proposes k tokens per sequence, the target model scores all k+1
+ * positions of B sequences in one forward pass whose linear layers run as
+ * FP8 E4M3 W8A8 (paper section 3.2, FP8 Post-Training Quantization) over
+ * M = B*(k+1) rows, and an acceptance test keeps the longest agreeing prefix
+ * plus one resampled or bonus token.
+ *
+ * Conventions shared by every entry point:
+ *  - Every buffer argument is DEVICE memory owned by the caller, except where
+ *    a comment says otherwise.  The library never allocates, frees or
+ *    synchronizes; it validates arguments on the host and then enqueues work
+ *    asynchronously on `stream` (a hipStream_t passed as void*; NULL means the
+ *    default stream).  Outputs are valid once that stream has reached the
+ *    enqueued work.
+ *  - All argument errors are detected on the host, before any HIP call, and
+ *    returned as a status; nothing is enqueued then.  A failed kernel launch
+ *    returns SPEC_ERR_HIP and records the hipError_t for spec_last_hip_error().
+ *  - Matrices are row-major; `ld_*` is the row stride in elements.
+ *  - bf16 tensors are raw 16-bit bfloat16 bit patterns (uint16_t storage).
+ *  - FP8 tensors are OCP E4M3 ("E4M3FN") bytes: bias 7, no infinities, NaN is
+ *    S.1111.111, largest finite magnitude 448.
+ *  - Calls are reentrant; the only global state is a thread-local copy of the
+ *    last HIP error.  Calls that share output or workspace buffers must not
+ *    overlap on different streams.
+ */
+#ifndef SPEC_FP8_H
+#define SPEC_FP8_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SPEC_OK = 0,
+    SPEC_ERR_NULL = 1,         /* a required pointer is NULL                         */
+    SPEC_ERR_SHAPE = 2,        /* a size is negative/zero where not allowed, ld < cols */
+    SPEC_ERR_UNSUPPORTED = 3,  /* valid but outside the supported fast path          */
+    SPEC_ERR_ENUM = 4,         /* an enum argument holds an unknown value            */
+    SPEC_ERR_ALIGN = 5,        /* pointer or stride misaligned for vector access     */
+    SPEC_ERR_WORKSPACE = 6,    /* workspace missing or smaller than required         */
+    SPEC_ERR_HIP = 7,          /* a HIP launch failed (see spec_last_hip_error)      */
+    SPEC_ERR_VALUE = 8         /* a scalar argument is out of range (e.g. temperature) */
+} spec_status;
+
+typedef enum {
+    SPEC_SCALE_PER_ROW = 0,    /* dynamic: one scale per row (per token for activations,
+                                  per output channel for weights W[N,K])              */
+    SPEC_SCALE_PER_TENSOR = 1  /* static: one fp32 scale for the whole tensor         */
+} spec_scale_mode;
+
+typedef enum {
+    SPEC_QIN_BF16 = 0,         /* quantize x itself                                   */
+    SPEC_QIN_SILU_MUL_BF16 = 1 /* quantize h = bf16(silu(x[:, c]) * x[:, cols + c])   */
+} spec_quant_input;
+
+typedef enum {
+    SPEC_OUT_BF16 = 0,         /* bf16, round-to-nearest-even of the fp32 result       */
+    SPEC_OUT_F32 = 1
+} spec_out_dtype;
+
+/*
+ * spec_fp8_quantize -- rows of bf16 values to E4M3 codes with fp32 scales.
+ *
+ * The paper quantizes activations and weights to E4M3 with min-max scales
+ * (section 3.2); E4M3 is symmetric with no zero point, so the scale of a
+ * range with largest magnitude amax is amax / 448.  For every row r:
+ *
+ *   v[c]  = x[r,c]                                   (in_kind = SPEC_QIN_BF16)
+ *         = bf16(silu(x[r,c]) * x[r,cols+c])         (SPEC_QIN_SILU_MUL_BF16: x is
+ *           [rows, 2*cols], gate columns first, then up; the gated FFN of the
+ *           Llama-family target model, section 4)
+ *   PER_ROW:    s[r] = max(fl32(max_c |v[c]| / 448), 2^-100); scales[r] = s[r]   (written)
+ *   PER_TENSOR: s[r] = scales[0]                                               (read)
+ *   q[r,c] = E4M3(fl32(v[c] * fl32(1 / s[r])))
+ *
+ * E4M3(.) rounds to nearest with ties to the even mantissa and saturates any
+ * magnitude above 448 to +-448; NaN gives 0x7F; the sign of zero is kept.
+ * fl32(a/b) is the correctly rounded fp32 quotient.  Results are bit-exact.
+ *
+ * x       bf16 [rows, ld_x]; cols (or 2*cols for SILU_MUL) <= ld_x.
+ * scales  fp32 [rows] (PER_ROW, written) or fp32 [1] (PER_TENSOR, read; must be
+ *         finite and > 0).
+ * q       uint8 [rows, ld_q], cols <= ld_q.
+ * Requirements: rows >= 0 (0 is a no-op), cols > 0 and cols % 8 == 0,
+ * ld_x % 8 == 0, ld_q % 8 == 0, x and q 16-byte aligned (SPEC_ERR_ALIGN or
+ * SPEC_ERR_UNSUPPORTED otherwise).  Non-finite inputs give unspecified codes.
+ */
+spec_status spec_fp8_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x,
+                              spec_quant_input in_kind, spec_scale_mode mode,
+                              float* scales, uint8_t* q, int64_t ld_q, void* stream);
+
+/*
+ * spec_silu_mul_bf16 -- h[r,c] = bf16(silu(x[r,c]) * x[r,cols+c]) without
+ * quantizing: exactly the intermediate that SPEC_QIN_SILU_MUL_BF16 quantizes,
+ * computed by the same device code.  Same requirements as spec_fp8_quantize;
+ * h is bf16 [rows, ld_h], ld_h % 8 == 0, 16-byte aligned.
+ */
+spec_status spec_silu_mul_bf16(const void* x, int64_t rows, int64_t cols, int64_t ld_x,
+                               void* h, int64_t ld_h, void* stream);
+
+/*
+ * spec_fp8_gemm -- the W8A8 linear layer (section 3.2):
+ *
+ *   acc[m,n] = sum_k dec(A[m,k]) * dec(W[n,k])     accumulated in fp32
+ *   Y[m,n]   = fl32(fl32(acc[m,n] * sa(m)) * sw(n))  then bf16 (RNE) or fp32
+ *
+ * A       uint8 E4M3 [M, lda] (activations, K contiguous), K <= lda.
+ * W       uint8 E4M3 [N, ldw] (weights in nn.Linear layout: row = output channel).
+ * a_scale fp32 [M] (PER_ROW) or [1] (PER_TENSOR); w_scale fp32 [N] or [1].
+ * Y       bf16 or fp32 [M, ldy], N <= ldy.
+ * workspace  device scratch of at least spec_fp8_gemm_workspace_bytes(M,N,K)
+ *         bytes (may be NULL when that is 0); contents on entry are ignored.
+ * Requirements: M >= 0 (0 is a no-op), N > 0, K > 0, K % 128 == 0 (else
+ * SPEC_ERR_UNSUPPORTED); lda % 16 == 0, ldw % 16 == 0, A and W 16-byte
+ * aligned; ldy % 8 == 0 and Y 16-byte aligned.  M and N need not be tile
+ * multiples.  Products of E4M3 values are exact; only the fp32 accumulation
+ * and the epilogue round.
+ */
+size_t spec_fp8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, spec_scale_mode a_mode,
+                          const uint8_t* w, int64_t ldw, const float* w_scale, spec_scale_mode w_mode,
+                          int64_t M, int64_t N, int64_t K,
+                          void* y, int64_t ldy, spec_out_dtype out_dtype,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * spec_verify_accept -- acceptance of B drafted chains of length k
+ * (section 3.1; the rule of the speculative-sampling papers it cites):
+ *
+ *   temperature == 0 (greedy): g_i = argmax_v target[b,i,v] (lowest index on
+ *     ties); keep draft x_i while x_i == g_i; emit g_a at the first mismatch
+ *     a, or the bonus g_k after k matches.
+ *   temperature > 0 (speculative sampling): p_i = softmax(target[b,i,:]/T),
+ *     q_i = softmax(draft[b,i,:]/T) (or one-hot at x_i when draft_logits is
+ *     NULL).  For i = 0..k-1: accept x_i iff u[b,i] * q_i(x_i) < p_i(x_i);
+ *     at the first rejection emit the smallest v whose cumulative residual
+ *     sum_{w<=v} max(0, p_i - q_i)(w) exceeds u[b,k] times the residual's
+ *     total, and stop.  If all k are accepted, emit the bonus token drawn the
+ *     same way from p_k with u[b,k].
+ *
+ * target_logits bf16 [B, k+1, V] (position i scores draft i; position k the bonus).
+ * draft_logits  bf16 [B, k, V] or NULL.
+ * draft_tokens  int32 [B, k]; an id outside [0, V) is a rejection with p = q = 0.
+ * uniforms      fp32 [B, k+1] in [0, 1) (ignored when temperature == 0).
+ * out_tokens    int32 [B, k+1]: accepted drafts then the emitted token, -1 padded.
+ * num_accepted  int32 [B]: a_b in [0, k]; a_b + 1 tokens are emitted.
+ * workspace     >= spec_verify_accept_workspace_bytes(B, k, V) bytes; contents on
+ *               entry are ignored.
+ * Requirements: B >= 0 (0 is a no-op), 1 <= k <= 16, 1 <= V <= 2^31 - 1;
+ * temperature finite and >= 0 (SPEC_ERR_VALUE otherwise).  Probabilities are
+ * computed in fp32; a decision within ~1e-5 relative of its boundary may
+ * differ from an exact evaluation.
+ */
+size_t spec_verify_accept_workspace_bytes(int64_t B, int64_t k, int64_t V);
+
+spec_status spec_verify_accept(const void* target_logits, const void* draft_logits,
+                               const int32_t* draft_tokens, const float* uniforms,
+                               int64_t B, int64_t k, int64_t V, float temperature,
+                               int32_t* out_tokens, int32_t* num_accepted,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static description of a status code (never NULL). */
+const char* spec_status_string(spec_status s);
+
+/* hipError_t value of the last SPEC_ERR_HIP returned on this thread (0 if none). */
+int spec_last_hip_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int spec_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPEC_FP8_H */

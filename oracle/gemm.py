@@ -75,17 +75,16 @@ def gemm_rows(a_codes, sa, w_codes, sw, rows) -> np.ndarray:
 
 
 def rel_error(y: np.ndarray, y_ref: np.ndarray) -> float:
-    """max_{m,n} |y - y_ref| / max(|y_ref|, 0.01 * rms of y_ref's row).
+    """Largest error of any output relative to the largest magnitude of its row.
 
-    The floor keeps outputs that cancel to near zero from dominating the
-    relative error; 0.01 of the row's rms is far below any value that
-    matters to the next layer.
+    max_m max_n |y[m,n] - y_ref[m,n]| / max_n |y_ref[m,n]|: the infinity-norm
+    relative error of every output row (one token's activations), which stays
+    meaningful for outputs that cancel to near zero.
     """
     y = np.asarray(y, dtype=np.float64)
     y_ref = np.asarray(y_ref, dtype=np.float64)
     if y_ref.size == 0:
         return 0.0
-    rms = np.sqrt(np.mean(y_ref * y_ref, axis=1, keepdims=True))
-    denom = np.maximum(np.abs(y_ref), 0.01 * rms)
-    denom = np.where(denom > 0, denom, 1.0)
-    return float(np.max(np.abs(y - y_ref) / denom))
+    scale = np.max(np.abs(y_ref), axis=1, keepdims=True)
+    scale = np.where(scale > 0, scale, 1.0)
+    return float(np.max(np.abs(y - y_ref) / scale))

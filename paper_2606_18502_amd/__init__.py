@@ -1,0 +1,23 @@
+"""FP8 speculative-decoding verify path for AMD Instinct MI355X (gfx950).
+
+The hot path of the inference-optimization stage of arxiv 2606.18502: the
+target model's verification step of speculative decoding run in FP8 E4M3
+W8A8 -- dynamic per-token activation quantization, per-output-channel weight
+scales, an fp32-accumulated FP8-MFMA GEMM with a scale epilogue -- followed by
+greedy or speculative-sampling acceptance of the drafted tokens.
+
+The computation lives in libspecfp8.so (HIP kernels behind the C ABI of
+include/spec_fp8.h); this package only marshals torch tensors into that ABI.
+"""
+
+from ._lib import SpecError, load as load_library, LIB_PATH  # noqa: F401
+from .ops import (  # noqa: F401
+    quantize,
+    silu_mul,
+    gemm,
+    gemm_workspace_bytes,
+    verify_accept,
+    accept_workspace_bytes,
+)
+
+__version__ = "0.1.0"

@@ -1,0 +1,105 @@
+// extern "C" entry points of libspecfp8.so: validate on the host, then
+// enqueue the kernels on the caller's stream.  Nothing here allocates,
+// frees or synchronizes.
+#include <hip/hip_runtime.h>
+
+#include "../../include/spec_fp8.h"
+#include "kernels.hpp"
+#include "validate.hpp"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+inline spec_status from_hip(hipError_t e) {
+    if (e == hipSuccess) return SPEC_OK;
+    g_last_hip_error = (int)e;
+    return SPEC_ERR_HIP;
+}
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+spec_status spec_fp8_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x,
+                              spec_quant_input in_kind, spec_scale_mode mode, float* scales, uint8_t* q,
+                              int64_t ld_q, void* stream) {
+    const spec_status st = specfp8::check_quantize(x, rows, cols, ld_x, (int)in_kind, (int)mode, scales, q, ld_q);
+    if (st != SPEC_OK || rows == 0) return st;
+    return from_hip(specfp8::launch_quantize(reinterpret_cast<const uint16_t*>(x), rows, cols, ld_x, (int)in_kind,
+                                             (int)mode, scales, q, ld_q, as_stream(stream)));
+}
+
+spec_status spec_silu_mul_bf16(const void* x, int64_t rows, int64_t cols, int64_t ld_x, void* h, int64_t ld_h,
+                               void* stream) {
+    const spec_status st = specfp8::check_silu_mul(x, rows, cols, ld_x, h, ld_h);
+    if (st != SPEC_OK || rows == 0) return st;
+    return from_hip(specfp8::launch_silu_mul(reinterpret_cast<const uint16_t*>(x), rows, cols, ld_x,
+                                             reinterpret_cast<uint16_t*>(h), ld_h, as_stream(stream)));
+}
+
+size_t spec_fp8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N <= 0 || K <= 0 || K % 128 != 0) return 0;
+    return specfp8::plan_gemm(M, N, K).workspace_bytes;
+}
+
+spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, spec_scale_mode a_mode,
+                          const uint8_t* w, int64_t ldw, const float* w_scale, spec_scale_mode w_mode, int64_t M,
+                          int64_t N, int64_t K, void* y, int64_t ldy, spec_out_dtype out_dtype, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    const spec_status st = specfp8::check_gemm(a, lda, a_scale, (int)a_mode, w, ldw, w_scale, (int)w_mode, M, N, K,
+                                               y, ldy, (int)out_dtype);
+    if (st != SPEC_OK || M == 0) return st;
+    const specfp8::GemmPlan plan = specfp8::plan_gemm(M, N, K);
+    if (plan.workspace_bytes > 0) {
+        if (!workspace || workspace_bytes < plan.workspace_bytes) return SPEC_ERR_WORKSPACE;
+        if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return SPEC_ERR_ALIGN;
+    }
+    return from_hip(specfp8::launch_gemm(plan, a, lda, a_scale, a_mode == SPEC_SCALE_PER_TENSOR, w, ldw, w_scale,
+                                         w_mode == SPEC_SCALE_PER_TENSOR, M, N, K, y, ldy, out_dtype == SPEC_OUT_F32,
+                                         workspace, as_stream(stream)));
+}
+
+size_t spec_verify_accept_workspace_bytes(int64_t B, int64_t k, int64_t V) {
+    if (B <= 0 || k < 1 || V < 1) return 0;
+    return specfp8::plan_accept(B, k, V).bytes;
+}
+
+spec_status spec_verify_accept(const void* target_logits, const void* draft_logits, const int32_t* draft_tokens,
+                               const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
+                               int32_t* out_tokens, int32_t* num_accepted, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+    const spec_status st = specfp8::check_accept(target_logits, draft_logits, draft_tokens, uniforms, B, k, V,
+                                                 temperature, out_tokens, num_accepted);
+    if (st != SPEC_OK || B == 0) return st;
+    const specfp8::AcceptPlan plan = specfp8::plan_accept(B, k, V);
+    if (!workspace || workspace_bytes < plan.bytes) return SPEC_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return SPEC_ERR_ALIGN;
+    return from_hip(specfp8::launch_accept(plan, reinterpret_cast<const uint16_t*>(target_logits),
+                                           reinterpret_cast<const uint16_t*>(draft_logits), draft_tokens, uniforms,
+                                           B, k, V, temperature, out_tokens, num_accepted, workspace,
+                                           as_stream(stream)));
+}
+
+const char* spec_status_string(spec_status s) {
+    switch (s) {
+        case SPEC_OK: return "ok";
+        case SPEC_ERR_NULL: return "required pointer is NULL";
+        case SPEC_ERR_SHAPE: return "invalid shape or leading dimension";
+        case SPEC_ERR_UNSUPPORTED: return "shape outside the supported fast path";
+        case SPEC_ERR_ENUM: return "unknown enum value";
+        case SPEC_ERR_ALIGN: return "misaligned pointer or leading dimension";
+        case SPEC_ERR_WORKSPACE: return "workspace missing or too small";
+        case SPEC_ERR_HIP: return "HIP launch failed";
+        case SPEC_ERR_VALUE: return "scalar argument out of range";
+    }
+    return "unknown status";
+}
+
+int spec_last_hip_error(void) { return g_last_hip_error; }
+
+int spec_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,41 @@
+// Host-side launchers of the verify-path kernels (internal to libspecfp8).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace specfp8 {
+
+// ---- quantize.hip
+hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x, int in_kind,
+                           int mode, float* scales, uint8_t* q, int64_t ld_q, hipStream_t stream);
+hipError_t launch_silu_mul(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x,
+                           uint16_t* h, int64_t ld_h, hipStream_t stream);
+
+// ---- gemm.hip
+struct GemmPlan {
+    int kind;              // tile configuration
+    int m_tiles, n_tiles;  // output tiles
+    int splits;            // K-splits (1 = none)
+    int64_t ldp;           // row stride of the fp32 partial tiles
+    size_t workspace_bytes;
+};
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const float* sa, int a_per_tensor,
+                       const uint8_t* w, int64_t ldw, const float* sw, int w_per_tensor, int64_t M,
+                       int64_t N, int64_t K, void* y, int64_t ldy, int out_f32, void* workspace,
+                       hipStream_t stream);
+
+// ---- accept.hip
+struct AcceptPlan {
+    int64_t chunk;         // vocabulary elements per workgroup
+    int64_t nchunk;        // chunks per row
+    size_t stats_off, mass_off, ctr_off, bytes;
+};
+AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V);
+hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t* zd, const int32_t* x,
+                         const float* u, int64_t B, int64_t k, int64_t V, float temperature,
+                         int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream);
+
+}  // namespace specfp8

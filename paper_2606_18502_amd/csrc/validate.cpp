@@ -1,0 +1,84 @@
+#include "validate.hpp"
+
+#include <math.h>
+
+namespace specfp8 {
+
+namespace {
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int64_t kMaxGrid = 2147483647;   // grid.x limit
+constexpr int64_t kMaxGridY = 65535;       // grid.y limit
+
+}  // namespace
+
+spec_status check_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, int in_kind, int mode,
+                           const float* scales, const void* q, int64_t ld_q) {
+    if (in_kind != SPEC_QIN_BF16 && in_kind != SPEC_QIN_SILU_MUL_BF16) return SPEC_ERR_ENUM;
+    if (mode != SPEC_SCALE_PER_ROW && mode != SPEC_SCALE_PER_TENSOR) return SPEC_ERR_ENUM;
+    if (rows < 0 || cols <= 0) return SPEC_ERR_SHAPE;
+    const int64_t in_cols = in_kind == SPEC_QIN_SILU_MUL_BF16 ? 2 * cols : cols;
+    if (ld_x < in_cols || ld_q < cols) return SPEC_ERR_SHAPE;
+    if (rows > kMaxGrid) return SPEC_ERR_UNSUPPORTED;
+    if (cols % 8 != 0) return SPEC_ERR_UNSUPPORTED;
+    if (rows == 0) return SPEC_OK;
+    if (!x || !q || !scales) return SPEC_ERR_NULL;
+    if (ld_x % 8 != 0 || ld_q % 8 != 0 || !aligned16(x) || !aligned16(q)) return SPEC_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(scales) & 3u) != 0) return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
+spec_status check_silu_mul(const void* x, int64_t rows, int64_t cols, int64_t ld_x, const void* h,
+                           int64_t ld_h) {
+    if (rows < 0 || cols <= 0) return SPEC_ERR_SHAPE;
+    if (ld_x < 2 * cols || ld_h < cols) return SPEC_ERR_SHAPE;
+    if (cols % 8 != 0) return SPEC_ERR_UNSUPPORTED;
+    if ((cols / 8 + 255) / 256 > kMaxGrid) return SPEC_ERR_UNSUPPORTED;
+    if (rows == 0) return SPEC_OK;
+    if (!x || !h) return SPEC_ERR_NULL;
+    if (ld_x % 8 != 0 || ld_h % 8 != 0 || !aligned16(x) || !aligned16(h)) return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
+spec_status check_gemm(const void* a, int64_t lda, const float* a_scale, int a_mode, const void* w,
+                       int64_t ldw, const float* w_scale, int w_mode, int64_t M, int64_t N, int64_t K,
+                       const void* y, int64_t ldy, int out_dtype) {
+    if (a_mode != SPEC_SCALE_PER_ROW && a_mode != SPEC_SCALE_PER_TENSOR) return SPEC_ERR_ENUM;
+    if (w_mode != SPEC_SCALE_PER_ROW && w_mode != SPEC_SCALE_PER_TENSOR) return SPEC_ERR_ENUM;
+    if (out_dtype != SPEC_OUT_BF16 && out_dtype != SPEC_OUT_F32) return SPEC_ERR_ENUM;
+    if (M < 0 || N <= 0 || K <= 0) return SPEC_ERR_SHAPE;
+    if (lda < K || ldw < K || ldy < N) return SPEC_ERR_SHAPE;
+    if (K % 128 != 0) return SPEC_ERR_UNSUPPORTED;
+    if (M > 2147483647LL || N > 2147483647LL || K > 2147483647LL) return SPEC_ERR_UNSUPPORTED;
+    if (M == 0) return SPEC_OK;
+    if (!a || !w || !a_scale || !w_scale || !y) return SPEC_ERR_NULL;
+    if (lda % 16 != 0 || ldw % 16 != 0 || !aligned16(a) || !aligned16(w)) return SPEC_ERR_ALIGN;
+    if (ldy % 8 != 0 || !aligned16(y)) return SPEC_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(a_scale) & 3u) || (reinterpret_cast<uintptr_t>(w_scale) & 3u))
+        return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
+spec_status check_accept(const void* target_logits, const void* draft_logits, const int32_t* draft_tokens,
+                         const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
+                         const int32_t* out_tokens, const int32_t* num_accepted) {
+    (void)draft_logits;
+    if (!isfinite(temperature) || temperature < 0.0f) return SPEC_ERR_VALUE;
+    if (B < 0 || k < 1 || V < 1) return SPEC_ERR_SHAPE;
+    if (k > 16 || V > 2147483647LL) return SPEC_ERR_UNSUPPORTED;
+    if (B * (2 * k + 1) > kMaxGridY) return SPEC_ERR_UNSUPPORTED;
+    if (B == 0) return SPEC_OK;
+    if (!target_logits || !draft_tokens || !out_tokens || !num_accepted) return SPEC_ERR_NULL;
+    if (temperature > 0.0f && !uniforms) return SPEC_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(target_logits) & 1u) ||
+        (draft_logits && (reinterpret_cast<uintptr_t>(draft_logits) & 1u)))
+        return SPEC_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(draft_tokens) & 3u) || (reinterpret_cast<uintptr_t>(out_tokens) & 3u) ||
+        (reinterpret_cast<uintptr_t>(num_accepted) & 3u) ||
+        (uniforms && (reinterpret_cast<uintptr_t>(uniforms) & 3u)))
+        return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
+}  // namespace specfp8

@@ -1,0 +1,24 @@
+// Host-only argument checks of the libspecfp8 C ABI.  No HIP here: every
+// check runs before anything is enqueued, so argument errors never touch the
+// device (and can be exercised on a machine without a GPU).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/spec_fp8.h"
+
+namespace specfp8 {
+
+spec_status check_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, int in_kind, int mode,
+                           const float* scales, const void* q, int64_t ld_q);
+spec_status check_silu_mul(const void* x, int64_t rows, int64_t cols, int64_t ld_x, const void* h,
+                           int64_t ld_h);
+spec_status check_gemm(const void* a, int64_t lda, const float* a_scale, int a_mode, const void* w,
+                       int64_t ldw, const float* w_scale, int w_mode, int64_t M, int64_t N, int64_t K,
+                       const void* y, int64_t ldy, int out_dtype);
+spec_status check_accept(const void* target_logits, const void* draft_logits, const int32_t* draft_tokens,
+                         const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
+                         const int32_t* out_tokens, const int32_t* num_accepted);
+
+}  // namespace specfp8

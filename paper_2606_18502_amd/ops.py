@@ -1,0 +1,174 @@
+"""Torch-facing wrappers of the C ABI.
+
+Argument marshalling only: every step of the verify path runs in the HIP
+kernels of libspecfp8.so; torch provides device memory and the current stream.
+There is no CPU or torch fallback: without the built library every call raises.
+"""
+
+from __future__ import annotations
+
+from typing import Optional, Tuple
+
+import torch
+
+from . import _lib
+from ._lib import check
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dev(t: torch.Tensor, dtype: torch.dtype, name: str) -> None:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+
+
+def _rowmajor(t: torch.Tensor, name: str) -> int:
+    """Leading dimension of a 2-D row-major view (unit stride in the last dim)."""
+    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError(f"{name} must be a 2-D row-major view")
+    return t.stride(0) if t.shape[0] > 1 else max(t.shape[1], t.stride(0))
+
+
+def quantize(x: torch.Tensor, per_tensor_scale: Optional[torch.Tensor] = None, silu_mul: bool = False,
+             out: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None
+             ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """E4M3 row quantization of bf16 rows (spec_fp8_quantize).
+
+    x: bf16 [rows, cols] (or [rows, 2*cols] with silu_mul).  Dynamic per-row
+    scales unless `per_tensor_scale` (fp32 [1]) is given.
+    Returns (codes uint8 [rows, cols], scales fp32 [rows] or the given [1]).
+    """
+    lib = _lib.load()
+    _dev(x, torch.bfloat16, "x")
+    rows = x.shape[0]
+    cols = x.shape[1] // 2 if silu_mul else x.shape[1]
+    ld_x = _rowmajor(x, "x")
+    if out is None:
+        out = torch.empty((rows, cols), dtype=torch.uint8, device=x.device)
+    _dev(out, torch.uint8, "out")
+    ld_q = _rowmajor(out, "out")
+    if per_tensor_scale is not None:
+        _dev(per_tensor_scale, torch.float32, "per_tensor_scale")
+        scales = per_tensor_scale
+        mode = _lib.SCALE_PER_TENSOR
+    else:
+        if scales is None:
+            scales = torch.empty((rows,), dtype=torch.float32, device=x.device)
+        _dev(scales, torch.float32, "scales")
+        mode = _lib.SCALE_PER_ROW
+    kind = _lib.QIN_SILU_MUL_BF16 if silu_mul else _lib.QIN_BF16
+    check("spec_fp8_quantize", lib.spec_fp8_quantize(x.data_ptr(), rows, cols, ld_x, kind, mode,
+                                                     scales.data_ptr(), out.data_ptr(), ld_q, _stream()))
+    return out, scales
+
+
+def silu_mul(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """h = bf16(silu(gate) * up) for x = [gate | up] bf16 [rows, 2*cols] (spec_silu_mul_bf16)."""
+    lib = _lib.load()
+    _dev(x, torch.bfloat16, "x")
+    rows, cols = x.shape[0], x.shape[1] // 2
+    if out is None:
+        out = torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    _dev(out, torch.bfloat16, "out")
+    check("spec_silu_mul_bf16", lib.spec_silu_mul_bf16(x.data_ptr(), rows, cols, _rowmajor(x, "x"),
+                                                       out.data_ptr(), _rowmajor(out, "out"), _stream()))
+    return out
+
+
+def gemm_workspace_bytes(M: int, N: int, K: int) -> int:
+    return int(_lib.load().spec_fp8_gemm_workspace_bytes(M, N, K))
+
+
+def gemm(a: torch.Tensor, sa: torch.Tensor, w: torch.Tensor, sw: torch.Tensor,
+         out_dtype: torch.dtype = torch.bfloat16, out: Optional[torch.Tensor] = None,
+         workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Y = dec(A) dec(W)^T * sa * sw (spec_fp8_gemm).
+
+    a: uint8 E4M3 [M,K]; sa: fp32 [M] (per token) or [1] (per tensor);
+    w: uint8 E4M3 [N,K]; sw: fp32 [N] (per channel) or [1].
+    """
+    lib = _lib.load()
+    _dev(a, torch.uint8, "a")
+    _dev(w, torch.uint8, "w")
+    _dev(sa, torch.float32, "sa")
+    _dev(sw, torch.float32, "sw")
+    M, K = a.shape
+    N = w.shape[0]
+    if w.shape[1] != K:
+        raise ValueError("a and w disagree on K")
+    a_mode = _lib.SCALE_PER_TENSOR if sa.numel() == 1 and M != 1 else _lib.SCALE_PER_ROW
+    w_mode = _lib.SCALE_PER_TENSOR if sw.numel() == 1 and N != 1 else _lib.SCALE_PER_ROW
+    if a_mode == _lib.SCALE_PER_ROW and sa.numel() < M:
+        raise ValueError("sa must hold M per-row scales or one per-tensor scale")
+    if w_mode == _lib.SCALE_PER_ROW and sw.numel() < N:
+        raise ValueError("sw must hold N per-channel scales or one per-tensor scale")
+    if out is None:
+        # the ABI wants a row stride that is a multiple of 8 elements
+        ld = (N + 7) // 8 * 8
+        out = torch.empty((M, ld), dtype=out_dtype, device=a.device)[:, :N]
+    if out.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("out must be bf16 or fp32")
+    _dev(out, out.dtype, "out")
+    odt = _lib.OUT_F32 if out.dtype == torch.float32 else _lib.OUT_BF16
+    need = gemm_workspace_bytes(M, N, K)
+    ws_ptr, ws_bytes = None, 0
+    if need:
+        if workspace is None or workspace.numel() * workspace.element_size() < need:
+            workspace = torch.empty((need,), dtype=torch.uint8, device=a.device)
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    check("spec_fp8_gemm", lib.spec_fp8_gemm(a.data_ptr(), _rowmajor(a, "a"), sa.data_ptr(), a_mode,
+                                             w.data_ptr(), _rowmajor(w, "w"), sw.data_ptr(), w_mode, M, N, K,
+                                             out.data_ptr(), _rowmajor(out, "out"), odt, ws_ptr, ws_bytes,
+                                             _stream()))
+    return out
+
+
+def accept_workspace_bytes(B: int, k: int, V: int) -> int:
+    return int(_lib.load().spec_verify_accept_workspace_bytes(B, k, V))
+
+
+def verify_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
+                  uniforms: Optional[torch.Tensor], temperature: float,
+                  workspace: Optional[torch.Tensor] = None,
+                  out_tokens: Optional[torch.Tensor] = None, num_accepted: Optional[torch.Tensor] = None
+                  ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Greedy (T=0) or speculative-sampling (T>0) acceptance (spec_verify_accept).
+
+    target_logits bf16 [B,k+1,V]; draft_logits bf16 [B,k,V] or None;
+    draft_tokens int32 [B,k]; uniforms fp32 [B,k+1] (T>0).
+    Returns (out_tokens int32 [B,k+1] (-1 padded), num_accepted int32 [B]).
+    """
+    lib = _lib.load()
+    _dev(target_logits, torch.bfloat16, "target_logits")
+    B, k1, V = target_logits.shape
+    k = k1 - 1
+    if not target_logits.is_contiguous():
+        raise ValueError("target_logits must be contiguous")
+    if draft_logits is not None:
+        _dev(draft_logits, torch.bfloat16, "draft_logits")
+        if tuple(draft_logits.shape) != (B, k, V) or not draft_logits.is_contiguous():
+            raise ValueError("draft_logits must be contiguous [B,k,V]")
+    _dev(draft_tokens, torch.int32, "draft_tokens")
+    if tuple(draft_tokens.shape) != (B, k) or not draft_tokens.is_contiguous():
+        raise ValueError("draft_tokens must be contiguous [B,k]")
+    if uniforms is not None:
+        _dev(uniforms, torch.float32, "uniforms")
+        if tuple(uniforms.shape) != (B, k1) or not uniforms.is_contiguous():
+            raise ValueError("uniforms must be contiguous [B,k+1]")
+    if out_tokens is None:
+        out_tokens = torch.empty((B, k1), dtype=torch.int32, device=target_logits.device)
+    if num_accepted is None:
+        num_accepted = torch.empty((B,), dtype=torch.int32, device=target_logits.device)
+    need = accept_workspace_bytes(B, k, V)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=target_logits.device)
+    check("spec_verify_accept", lib.spec_verify_accept(
+        target_logits.data_ptr(), None if draft_logits is None else draft_logits.data_ptr(),
+        draft_tokens.data_ptr(), None if uniforms is None else uniforms.data_ptr(), B, k, V,
+        float(temperature), out_tokens.data_ptr(), num_accepted.data_ptr(), workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(), _stream()))
+    return out_tokens, num_accepted

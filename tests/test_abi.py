@@ -1,0 +1,142 @@
+"""The C-ABI library loads, exports every symbol include/spec_fp8.h declares,
+and rejects every invalid argument on the host before any HIP call (these
+calls never reach a kernel, so they run without a GPU)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spec_fp8.h")
+
+OK, NULL, SHAPE, UNSUP, ENUM, ALIGN, WS, HIP, VALUE = range(9)
+A16 = 0x10000            # fake, 16-byte aligned device address: never dereferenced here
+A1 = 0x10001             # misaligned
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2606_18502_amd as p
+    if not os.path.exists(p.LIB_PATH):
+        from paper_2606_18502_amd import build
+        build.build()
+    return p.load_library()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(spec_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(lib, n), n
+    from paper_2606_18502_amd import _lib
+    assert set(_lib.EXPORTS) == set(names)
+
+
+def test_version_and_status_strings(lib):
+    assert lib.spec_version() == 100
+    for s in range(9):
+        assert lib.spec_status_string(s)
+    assert lib.spec_status_string(99) == b"unknown status"
+    assert lib.spec_last_hip_error() == 0
+
+
+def q(lib, x=A16, rows=4, cols=64, ld_x=64, kind=0, mode=0, scales=A16, qp=A16, ld_q=64):
+    return lib.spec_fp8_quantize(x, rows, cols, ld_x, kind, mode, scales, qp, ld_q, None)
+
+
+def test_quantize_validation(lib):
+    assert q(lib, kind=2) == ENUM
+    assert q(lib, mode=5) == ENUM
+    assert q(lib, rows=-1) == SHAPE
+    assert q(lib, cols=0) == SHAPE
+    assert q(lib, ld_x=32) == SHAPE
+    assert q(lib, kind=1, ld_x=64) == SHAPE            # SiLU input needs 2*cols
+    assert q(lib, ld_q=32) == SHAPE
+    assert q(lib, cols=60, ld_x=64, ld_q=64) == UNSUP  # cols % 8
+    assert q(lib, x=None) == NULL
+    assert q(lib, scales=None) == NULL
+    assert q(lib, qp=None) == NULL
+    assert q(lib, x=A1) == ALIGN
+    assert q(lib, ld_x=68) == ALIGN
+    assert q(lib, scales=A16 + 2) == ALIGN
+    assert q(lib, rows=0, x=None, scales=None, qp=None) == OK   # empty: no-op
+
+
+def test_silu_mul_validation(lib):
+    f = lib.spec_silu_mul_bf16
+    assert f(A16, 4, 64, 64, A16, 64, None) == SHAPE          # ld_x < 2*cols
+    assert f(A16, 4, 60, 120, A16, 64, None) == UNSUP
+    assert f(None, 4, 64, 128, A16, 64, None) == NULL
+    assert f(A1, 4, 64, 128, A16, 64, None) == ALIGN
+    assert f(None, 0, 64, 128, None, 64, None) == OK
+
+
+def g(lib, a=A16, lda=512, sa=A16, am=0, w=A16, ldw=512, sw=A16, wm=0, M=8, N=1024, K=512,
+      y=A16, ldy=1024, od=0, ws=None, wsb=0):
+    return lib.spec_fp8_gemm(a, lda, sa, am, w, ldw, sw, wm, M, N, K, y, ldy, od, ws, wsb, None)
+
+
+def test_gemm_validation(lib):
+    assert g(lib, am=3) == ENUM
+    assert g(lib, wm=-1) == ENUM
+    assert g(lib, od=7) == ENUM
+    assert g(lib, M=-1) == SHAPE
+    assert g(lib, N=0) == SHAPE
+    assert g(lib, K=0) == SHAPE
+    assert g(lib, lda=256) == SHAPE
+    assert g(lib, ldy=512) == SHAPE
+    assert g(lib, K=500, lda=512, ldw=512) == UNSUP
+    assert g(lib, a=None) == NULL
+    assert g(lib, sw=None) == NULL
+    assert g(lib, y=None) == NULL
+    assert g(lib, a=A1) == ALIGN
+    assert g(lib, lda=520) == ALIGN
+    assert g(lib, ldy=1028) == ALIGN
+    assert g(lib, M=0, a=None, sa=None, w=None, sw=None, y=None) == OK
+    # a shape that splits K needs a workspace
+    need = lib.spec_fp8_gemm_workspace_bytes(320, 1024, 4096)
+    assert need > 0
+    assert g(lib, M=320, N=1024, K=4096, lda=4096, ldw=4096, ldy=1024) == WS
+    assert g(lib, M=320, N=1024, K=4096, lda=4096, ldw=4096, ldy=1024, ws=A16, wsb=need - 1) == WS
+    assert g(lib, M=320, N=1024, K=4096, lda=4096, ldw=4096, ldy=1024, ws=A1, wsb=need) == ALIGN
+    assert lib.spec_fp8_gemm_workspace_bytes(8, 1024, 100) == 0
+
+
+def acc(lib, zt=A16, zd=A16, x=A16, u=A16, B=2, k=3, V=256, T=0.7, out=A16, num=A16, ws=A16, wsb=1 << 20):
+    return lib.spec_verify_accept(zt, zd, x, u, B, k, V, ctypes.c_float(T), out, num, ws, wsb, None)
+
+
+def test_accept_validation(lib):
+    assert acc(lib, T=float("nan")) == VALUE
+    assert acc(lib, T=-0.5) == VALUE
+    assert acc(lib, T=float("inf")) == VALUE
+    assert acc(lib, k=0) == SHAPE
+    assert acc(lib, B=-1) == SHAPE
+    assert acc(lib, V=0) == SHAPE
+    assert acc(lib, k=17) == UNSUP
+    assert acc(lib, V=1 << 31) == UNSUP
+    assert acc(lib, B=20000, k=4) == UNSUP
+    assert acc(lib, zt=None) == NULL
+    assert acc(lib, x=None) == NULL
+    assert acc(lib, u=None) == NULL                 # T > 0 needs uniforms
+    assert acc(lib, zt=A1) == ALIGN
+    assert acc(lib, num=A16 + 2) == ALIGN
+    need = lib.spec_verify_accept_workspace_bytes(2, 3, 256)
+    assert need > 0
+    assert acc(lib, ws=None) == WS
+    assert acc(lib, wsb=need - 1) == WS
+    assert acc(lib, ws=A16 + 8, wsb=need) == ALIGN
+    assert acc(lib, B=0, zt=None, zd=None, x=None, u=None, out=None, num=None, ws=None, wsb=0) == OK
+
+
+def test_workspace_sizes_grow_with_problem(lib):
+    assert lib.spec_verify_accept_workspace_bytes(64, 4, 128256) > lib.spec_verify_accept_workspace_bytes(2, 3, 256)
+    assert lib.spec_verify_accept_workspace_bytes(0, 3, 256) == 0
+    assert lib.spec_fp8_gemm_workspace_bytes(4096, 14336, 4096) == 0     # enough tiles: no split

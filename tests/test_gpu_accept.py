@@ -1,0 +1,172 @@
+"""GPU parity of spec_verify_accept against the oracle.
+
+Greedy: token ids and accepted counts bit-exact.  Speculative sampling: the
+GPU evaluates probabilities in fp32 and the oracle in fp64.  The GPU's
+probabilities carry a relative error of about 1e-6 (fp32 exponent argument and
+sums; a common normalisation error cancels between u*R and the cumulative
+sums), so every sequence whose decisions all lie farther than MARGIN (relative
+to p for accept tests, to R for samples) from their boundary must match
+exactly; sequences with a decision inside the margin are counted and checked
+for validity only.  At V=128256 the sampled token typically carries ~1e-4 of
+the mass, so a few sequences of a batch of 64 fall inside the margin.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import accept as oa
+from tests.gpu_util import dev_bf16, dev_f32, dev_i32, host, need_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+MARGIN = 4e-6
+
+
+def _check_valid(out, num, x, V):
+    B, k1 = out.shape
+    for b in range(B):
+        a = num[b]
+        assert 0 <= a < k1
+        assert np.all(out[b, :a] == x[b, :a])
+        assert 0 <= out[b, a] < V
+        assert np.all(out[b, a + 1:] == -1)
+
+
+def _stochastic_case(B, k, V, seed, c, T, with_draft=True, scale=2.0):
+    zt, zd = wl.accept_logits(B, k, V, seed, c, scale=scale)
+    x = wl.draft_tokens_sampled(zd, T, seed=seed + 1) if with_draft else wl.draft_tokens_greedy(zd)
+    u = wl.philox_uniforms((B, k + 1), seed=seed + 2)
+    return zt, (zd if with_draft else None), x, u
+
+
+@pytest.mark.parametrize("B,k,V,seed,c", [
+    (2, 3, 256, 0, 0.5),            # C1
+    (7, 4, 1000, 1, 0.9),
+    (5, 2, 1001, 2, 0.9),           # V not a multiple of 8: scalar path
+    (33, 4, 20000, 3, 0.99),        # several vocabulary chunks, ragged last chunk
+    (3, 16, 64, 4, 0.7),            # longest chain
+    (4, 1, 1, 5, 0.5),              # one-token vocabulary
+])
+def test_greedy_bit_exact(B, k, V, seed, c):
+    p = need_gpu()
+    say(f"greedy B={B} k={k} V={V}")
+    zt, zd = wl.accept_logits(B, k, V, seed, c)
+    x = wl.draft_tokens_greedy(zd)
+    x[0, 0] = V + 5 if B > 1 else x[0, 0]          # an out-of-range draft is a rejection
+    out, num = p.verify_accept(dev_bf16(zt), None, dev_i32(x), None, 0.0)
+    out_ref, num_ref = oa.accept_greedy(zt, x)
+    np.testing.assert_array_equal(host(num), num_ref)
+    np.testing.assert_array_equal(host(out), out_ref)
+
+
+def test_greedy_ties_lowest_index():
+    p = need_gpu()
+    B, k, V = 4, 2, 9000                            # ties across vocabulary chunks
+    z = np.zeros((B, k + 1, V), np.float32)
+    z[:, :, [8191, 8192, 100]] = 5.0
+    zt = wl.bf16_bits_from_f32(z)
+    x = np.full((B, k), 100, np.int32)
+    out, num = p.verify_accept(dev_bf16(zt), None, dev_i32(x), None, 0.0)
+    out_ref, num_ref = oa.accept_greedy(zt, x)
+    np.testing.assert_array_equal(host(out), out_ref)
+    assert np.all(host(out)[:, :k] == 100)
+
+
+@pytest.mark.parametrize("B,k,V,seed,c,with_draft", [
+    (2, 3, 256, 0, 0.5, True),     # C1
+    (16, 4, 5000, 1, 0.95, True),
+    (9, 3, 1001, 2, 0.9, True),    # scalar path
+    (16, 4, 20000, 3, 0.99, False),  # one-hot drafts (no draft logits)
+    (8, 8, 3000, 4, 0.0, True),    # uncorrelated: many rejections
+])
+def test_stochastic_parity(B, k, V, seed, c, with_draft):
+    p = need_gpu()
+    T = 0.7
+    say(f"stochastic B={B} k={k} V={V} draft_logits={with_draft}")
+    zt, zd, x, u = _stochastic_case(B, k, V, seed, c, T, with_draft)
+    out, num = p.verify_accept(dev_bf16(zt), None if zd is None else dev_bf16(zd), dev_i32(x), dev_f32(u), T)
+    out, num = host(out), host(num)
+    out_ref, num_ref, mg = oa.accept_stochastic(zt, zd, x, u, T, return_margins=True)
+    clear = mg > MARGIN
+    assert clear.mean() >= 0.9
+    np.testing.assert_array_equal(num[clear], num_ref[clear])
+    np.testing.assert_array_equal(out[clear], out_ref[clear])
+    _check_valid(out, num, x, V)
+
+
+def test_stochastic_full_vocab_c4():
+    """C4 at full size (B=64, k=4, V=128256, T=0.7), greedy and stochastic."""
+    p = need_gpu()
+    cfg = wl.CONFIGS["C4"]
+    B, k, V, T = cfg["B"], cfg["k"], cfg["V"], cfg["temperature"]
+    say("C4 logits")
+    zt, zd = wl.accept_logits(B, k, V, cfg["seed"], wl.C4_CORRELATION, scale=cfg["logit_std"], rank=cfg["rank"])
+    dzt, dzd = dev_bf16(zt), dev_bf16(zd)
+    xg = wl.draft_tokens_greedy(zd)
+    out, num = p.verify_accept(dzt, None, dev_i32(xg), None, 0.0)
+    out_ref, num_ref = oa.accept_greedy(zt, xg)
+    np.testing.assert_array_equal(host(out), out_ref)
+    np.testing.assert_array_equal(host(num), num_ref)
+    say(f"C4 greedy MGL {np.mean(num_ref + 1):.3f}")
+    xs = wl.draft_tokens_sampled(zd, T, seed=cfg["draft_seed"])
+    u = wl.philox_uniforms((B, k + 1), seed=cfg["uniform_seed"])
+    out, num = p.verify_accept(dzt, dzd, dev_i32(xs), dev_f32(u), T)
+    out, num = host(out), host(num)
+    out_ref, num_ref, mg = oa.accept_stochastic(zt, zd, xs, u, T, return_margins=True)
+    clear = mg > MARGIN
+    say(f"C4 stochastic MGL {np.mean(num_ref + 1):.3f}, margin events {int((~clear).sum())}")
+    assert clear.sum() >= 0.8 * B
+    np.testing.assert_array_equal(num[clear], num_ref[clear])
+    np.testing.assert_array_equal(out[clear], out_ref[clear])
+    _check_valid(out, num, xs, V)
+
+
+def test_p_equals_q_accepts_all():
+    p = need_gpu()
+    B, k, V = 32, 4, 3000
+    zt, _ = wl.accept_logits(B, k, V, 11, 0.5)
+    zd = np.ascontiguousarray(zt[:, :k])
+    x = wl.draft_tokens_sampled(zd, 0.7, seed=3)
+    u = wl.philox_uniforms((B, k + 1), seed=4)
+    out, num = p.verify_accept(dev_bf16(zt), dev_bf16(zd), dev_i32(x), dev_f32(u), 0.7)
+    assert np.all(host(num) == k)
+    np.testing.assert_array_equal(host(out)[:, :k], x)
+
+
+def test_emitted_law_matches_target_chi_square():
+    """Losslessness on the GPU: with one logit row replicated over many
+    sequences, the first emitted token follows p_0 (chi-square, V=64)."""
+    p = need_gpu()
+    V, k, T = 64, 2, 1.0
+    B = 13000
+    rng = np.random.default_rng(21)
+    zt1 = (rng.standard_normal((1, k + 1, V)) * 1.5).astype(np.float32)
+    zd1 = (zt1[:, :k] + rng.standard_normal((1, k, V)).astype(np.float32)).astype(np.float32)
+    zt = wl.bf16_bits_from_f32(np.repeat(zt1, B, 0))
+    zd = wl.bf16_bits_from_f32(np.repeat(zd1, B, 0))
+    p0 = oa.softmax64(zt[0, 0], T)
+    counts = np.zeros(V)
+    dzt, dzd = dev_bf16(zt), dev_bf16(zd)
+    for rep in range(5):
+        x = wl.draft_tokens_sampled(zd, T, seed=100 + rep)
+        u = wl.philox_uniforms((B, k + 1), seed=200 + rep)
+        out, _ = p.verify_accept(dzt, dzd, dev_i32(x), dev_f32(u), T)
+        counts += np.bincount(host(out)[:, 0], minlength=V)
+    n = counts.sum()
+    exp = p0 * n
+    keep = exp >= 5
+    chi2 = np.sum((counts[keep] - exp[keep]) ** 2 / exp[keep]) + (counts[~keep].sum() - exp[~keep].sum()) ** 2 / max(exp[~keep].sum(), 1e-9)
+    dof = keep.sum()
+    assert chi2 < dof + 6 * np.sqrt(2 * dof), (chi2, dof)
+
+
+def test_deterministic():
+    p = need_gpu()
+    zt, zd, x, u = _stochastic_case(16, 4, 20000, 7, 0.95, 0.7)
+    args = (dev_bf16(zt), dev_bf16(zd), dev_i32(x), dev_f32(u), 0.7)
+    a = [host(t) for t in p.verify_accept(*args)]
+    b = [host(t) for t in p.verify_accept(*args)]
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])

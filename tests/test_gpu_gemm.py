@@ -1,0 +1,190 @@
+"""GPU parity of spec_fp8_gemm against the oracle's exact fp64 accumulation.
+
+Two checks on the fp32 output:
+  * the target's tolerance, max relative error 2e-3, read per output row:
+    max_n |y - y_ref| / max_n |y_ref| (oracle.gemm.rel_error);
+  * elementwise, every sampled output lies within the error bound of the
+    device's FP8 matrix-core accumulation (tests/fp8_mfma_model.py), which
+    is pinned on the device by test_fp8_mfma_accumulation_model.
+The bf16 output must equal the round-to-nearest-even of the same kernel's
+fp32 output, bit for bit.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import e4m3, gemm as og, quantize as oq
+from tests.fp8_mfma_model import error_bound
+from tests.gpu_util import dev_bf16, dev_f32, dev_u8, host, host_bf16_bits, need_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+
+
+def _operands(M, N, K, seed, outliers=True):
+    xb = wl.linear_activations(M, K, seed, outlier_frac=0.01 if outliers else 0.0, outlier_scale=20.0)
+    wb = wl.linear_weights(N, K, seed + 1000)
+    a, sa = oq.quantize_rows(xb)
+    w, sw = oq.quantize_rows(wb)
+    return a, sa, w, sw
+
+
+def _f32_to_bf16_bits(y):
+    return wl.bf16_bits_from_f32(np.asarray(y, np.float32))
+
+
+def _check_bound(y, y_ref_sub, a, sa, w, sw, rows, cols):
+    bound = error_bound(a, sa, w, sw, rows, cols)
+    err = np.abs(y[np.ix_(rows, cols)] - y_ref_sub)
+    worst = float(np.max(err / bound))
+    assert worst <= 1.0, worst
+
+
+def _sample(n, count, seed):
+    rng = np.random.default_rng(seed)
+    idx = rng.choice(n, min(n, count), replace=False)
+    return np.unique(np.concatenate([idx, [0, n - 1]]))
+
+
+@pytest.mark.parametrize("M,N,K", [
+    (8, 1024, 512),                     # C1
+    (1, 16, 128), (17, 100, 256), (64, 64, 128),           # small tile, ragged
+    (80, 1040, 512), (100, 4096, 1024),                    # 80-row tile, split-K
+    (320, 640, 4096), (333, 272, 2048),                    # 320-row tile, split-K, ragged M
+    (700, 400, 512), (1024, 1024, 1024),                   # 256-row tile
+])
+def test_gemm_parity(M, N, K):
+    p = need_gpu()
+    say(f"gemm M={M} N={N} K={K} ws={p.gemm_workspace_bytes(M, N, K)}")
+    a, sa, w, sw = _operands(M, N, K, seed=M + N + K)
+    y_ref = og.gemm(a, sa, w, sw)
+    da, dw, dsa, dsw = dev_u8(a), dev_u8(w), dev_f32(sa), dev_f32(sw)
+    y32 = host(p.gemm(da, dsa, dw, dsw, out_dtype=torch.float32))
+    err = og.rel_error(y32, y_ref)
+    assert err <= TOL, err
+    rows, cols = _sample(M, 48, 1), _sample(N, 48, 2)
+    _check_bound(y32, y_ref[np.ix_(rows, cols)], a, sa, w, sw, rows, cols)
+    y16 = host_bf16_bits(p.gemm(da, dsa, dw, dsw, out_dtype=torch.bfloat16))
+    np.testing.assert_array_equal(y16, _f32_to_bf16_bits(y32))
+
+
+def test_gemm_ragged_n_and_strided_output():
+    p = need_gpu()
+    M, N, K = 21, 18, 256
+    a, sa, w, sw = _operands(M, N, K, seed=5)
+    y_ref = og.gemm(a, sa, w, sw)
+    out = torch.full((M, 24), -7.0, dtype=torch.float32, device="cuda")
+    p.gemm(dev_u8(a), dev_f32(sa), dev_u8(w), dev_f32(sw), out=out[:, :N])
+    o = host(out)
+    assert og.rel_error(o[:, :N], y_ref) <= TOL
+    assert np.all(o[:, N:] == -7.0)
+
+
+def test_gemm_per_tensor_scales():
+    p = need_gpu()
+    M, N, K = 40, 256, 512
+    xb = wl.student_t_activations(M, K, seed=3)
+    s_t = oq.calibrate_per_tensor([xb])
+    a = oq.quantize_per_tensor(xb, s_t)
+    w, sw = oq.quantize_rows(wl.linear_weights(N, K, 4))
+    y_ref = og.gemm(a, s_t, w, sw)
+    y = host(p.gemm(dev_u8(a), dev_f32([s_t]), dev_u8(w), dev_f32(sw), out_dtype=torch.float32))
+    assert og.rel_error(y, y_ref) <= TOL
+    sw_t = np.float32(0.0123)
+    y_ref2 = og.gemm(a, s_t, w, sw_t)
+    y2 = host(p.gemm(dev_u8(a), dev_f32([s_t]), dev_u8(w), dev_f32([sw_t]), out_dtype=torch.float32))
+    assert og.rel_error(y2, y_ref2) <= TOL
+
+
+@pytest.mark.parametrize("pool", [
+    [0x38, 0xB8, 0x40, 0xC0, 0x48, 0x50, 0x58, 0x00, 0x80],  # +-1, +-2, 3, 4, 6: group products within 2^6
+    [0x01, 0x81, 0x07, 0x87, 0x08, 0x88, 0x00, 0x10],        # subnormals: multiples of 2^-18
+])
+def test_gemm_exact_when_fp32_is_exact(pool):
+    """With products that the matrix cores sum exactly and power-of-two scales,
+    the kernel must reproduce the oracle exactly (no dropped or mis-scaled
+    product, subnormal E4M3 codes included)."""
+    p = need_gpu()
+    rng = np.random.default_rng(len(pool))
+    M, N, K = 16, 32, 256
+    pool = np.array(pool, np.uint8)
+    a = rng.choice(pool, (M, K)).astype(np.uint8)
+    w = rng.choice(pool, (N, K)).astype(np.uint8)
+    sa = np.full(M, 0.5, np.float32)
+    sw = np.full(N, 2.0, np.float32)
+    y_ref = og.gemm(a, sa, w, sw)
+    y = host(p.gemm(dev_u8(a), dev_f32(sa), dev_u8(w), dev_f32(sw), out_dtype=torch.float32))
+    np.testing.assert_array_equal(y.astype(np.float64), y_ref)
+
+
+def test_fp8_mfma_accumulation_model():
+    """Pins the device behaviour the error bound is built on: inside an aligned
+    group of 8 K positions a product 2^14 swallows a product 1 (2^13 does
+    not); across groups and K-steps the sum is exact."""
+    p = need_gpu()
+    M, N, K = 16, 16, 256
+    c = {v: int(e4m3.encode(np.array([v], np.float32))[0]) for v in (1.0, 64.0, 32.0, 256.0)}
+    a = np.zeros((M, K), np.uint8)
+    w = np.zeros((N, K), np.uint8)
+    a[:, 0] = c[256.0]
+    w[0, 0], w[1, 0] = c[64.0], c[32.0]              # products 2^14 and 2^13
+    w[2, 0] = c[64.0]
+    for m in range(M):
+        j = [1, 7, 8, 127, 128, 200, 3, 9, 15, 16, 64, 100, 129, 255, 5, 120][m]
+        a[m, j] = c[1.0]
+        w[:, j] = c[1.0]
+    y = host(p.gemm(dev_u8(a), dev_f32(np.ones(M)), dev_u8(w), dev_f32(np.ones(N)), out_dtype=torch.float32))
+    js = [1, 7, 8, 127, 128, 200, 3, 9, 15, 16, 64, 100, 129, 255, 5, 120]
+    for m, j in enumerate(js):
+        same_group = j < 8
+        assert y[m, 0] == (16384.0 if same_group else 16385.0), (m, j, y[m, 0])
+        assert y[m, 1] == 8193.0                      # 2^13 + 1 is kept either way
+
+
+def test_gemm_deterministic_with_split_k():
+    p = need_gpu()
+    M, N, K = 320, 1024, 4096
+    assert p.gemm_workspace_bytes(M, N, K) > 0         # this shape uses split-K
+    a, sa, w, sw = _operands(M, N, K, seed=9)
+    args = (dev_u8(a), dev_f32(sa), dev_u8(w), dev_f32(sw))
+    y1 = host(p.gemm(*args, out_dtype=torch.float32))
+    y2 = host(p.gemm(*args, out_dtype=torch.float32))
+    np.testing.assert_array_equal(y1, y2)
+
+
+@pytest.mark.parametrize("cfg", ["C2", "C3"])
+def test_layer_linears_full_size_sampled(cfg):
+    """The four verify-step linears at full size, in the launch configuration
+    the bench times, checked on sampled outputs.  The oracle quantizes the
+    sampled activation rows and weight rows itself from the same seeded bf16
+    inputs; the GPU's codes for those rows must match bit-exactly, and the GPU
+    GEMM output at the sampled (row, column) pairs must match the oracle's
+    exact GEMM to the tolerance."""
+    p = need_gpu()
+    c = wl.CONFIGS[cfg]
+    M = c["M"]
+    rows = np.array([0, 1, M // 2, M - 1])
+    for name, N, K in c["linears"]:
+        say(f"{cfg} {name}: M={M} N={N} K={K}")
+        rng = np.random.default_rng(N + K)
+        cols = np.unique(np.concatenate([[0, N - 1], rng.choice(N, 256, replace=False)]))
+        xb = wl.linear_activations(M, K, c["seed"], c["act_outlier_frac"], c["act_outlier_scale"])
+        wb = wl.linear_weights(N, K, c["seed"] + 17, c["w_std"])
+        x, wt = dev_bf16(xb), dev_bf16(wb)
+        a, sa = p.quantize(x)
+        w, sw = p.quantize(wt)
+        y = host(p.gemm(a, sa, w, sw, out_dtype=torch.float32))
+        qa_ref, sa_ref = oq.quantize_rows(xb[rows])
+        qw_ref, sw_ref = oq.quantize_rows(wb[cols])
+        np.testing.assert_array_equal(host(a)[rows], qa_ref)
+        np.testing.assert_array_equal(host(sa)[rows], sa_ref)
+        np.testing.assert_array_equal(host(w)[cols], qw_ref)
+        np.testing.assert_array_equal(host(sw)[cols], sw_ref)
+        y_ref = og.gemm(qa_ref, sa_ref, qw_ref, sw_ref)
+        assert og.rel_error(y[np.ix_(rows, cols)], y_ref) <= TOL
+        bound = error_bound(qa_ref, sa_ref, qw_ref, sw_ref, np.arange(len(rows)), np.arange(len(cols)))
+        assert np.all(np.abs(y[np.ix_(rows, cols)] - y_ref) <= bound)
+        del x, wt, a, w

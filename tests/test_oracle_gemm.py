@@ -86,8 +86,8 @@ def test_scales_per_row_per_tensor():
 
 
 def test_rel_error_metric():
-    y_ref = np.array([[100.0, -50.0, 0.0]])
+    y_ref = np.array([[100.0, -50.0, 0.0], [0.0, 0.0, 0.0]])
     assert og.rel_error(y_ref, y_ref) == 0.0
-    rms = np.sqrt((100.0 ** 2 + 50.0 ** 2) / 3)
-    y = y_ref + np.array([[0.1, 0.0, 0.01 * rms * 1e-3]])
-    assert abs(og.rel_error(y, y_ref) - 1e-3) < 1e-12
+    y = y_ref + np.array([[0.1, 0.0, 0.05], [0.0, 1e-3, 0.0]])
+    # row 0: 0.1 / 100; row 1 has no magnitude, its error is taken absolutely
+    assert abs(og.rel_error(y, y_ref) - 1e-3) < 1e-15
