@@ -154,7 +154,8 @@ spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, s
  * num_accepted  int32 [B]: a_b in [0, k]; a_b + 1 tokens are emitted.
  * workspace     >= spec_verify_accept_workspace_bytes(B, k, V) bytes; contents on
  *               entry are ignored.
- * Requirements: B >= 0 (0 is a no-op), 1 <= k <= 16, 1 <= V <= 2^31 - 1;
+ * Requirements: B >= 0 (0 is a no-op), 1 <= k <= 16, 1 <= V <= 2^23 and
+ * B*(2k+1) <= 65535 (SPEC_ERR_UNSUPPORTED otherwise);
  * temperature finite and >= 0 (SPEC_ERR_VALUE otherwise).  Probabilities are
  * computed in fp32; a decision within ~1e-5 relative of its boundary may
  * differ from an exact evaluation.

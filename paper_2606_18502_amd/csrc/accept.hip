@@ -27,8 +27,9 @@ namespace specfp8 {
 namespace {
 
 constexpr int kAThreads = 256;
-constexpr int kPerThread = 32;                        // elements per thread per chunk
-constexpr int64_t kChunk = kAThreads * kPerThread;    // 8192
+constexpr int kPerThread = 128;                       // elements per thread per chunk
+constexpr int64_t kChunk = kAThreads * kPerThread;    // 32768
+constexpr int kMaxChunks = 1024;                      // V <= 32M
 
 struct AcceptArgs {
     const uint16_t* zt;
@@ -79,12 +80,19 @@ __global__ __launch_bounds__(kAThreads) void greedy_partial_kernel(AcceptArgs a)
     const int64_t e1 = min(e0 + a.chunk, a.V);
     float bv = -INFINITY;
     int bi = 0x7fffffff;
+    uint4 raw[kPerThread / 8];
+#pragma unroll
+    for (int j = 0; j < kPerThread / 8; ++j) {           // all loads in flight first
+        const int64_t e = e0 + ((int64_t)j * kAThreads + threadIdx.x) * 8;
+        if (VEC && e < e1) raw[j] = *reinterpret_cast<const uint4*>(z + e);
+    }
 #pragma unroll
     for (int j = 0; j < kPerThread / 8; ++j) {
         const int64_t e = e0 + ((int64_t)j * kAThreads + threadIdx.x) * 8;
         if (e < e1) {
             float v[8];
-            load8<VEC>(z, e, a.V, v, -INFINITY);
+            if (VEC) unpack8(raw[j], v);
+            else load8<false>(z, e, a.V, v, -INFINITY);
 #pragma unroll
             for (int q = 0; q < 8; ++q)
                 if (e + q < e1 && better(v[q], (int)(e + q), bv, bi)) { bv = v[q]; bi = (int)(e + q); }
@@ -106,32 +114,37 @@ __global__ __launch_bounds__(kAThreads) void greedy_partial_kernel(AcceptArgs a)
     }
 }
 
-__global__ __launch_bounds__(64) void greedy_final_kernel(AcceptArgs a) {
+__global__ __launch_bounds__(256) void greedy_final_kernel(AcceptArgs a) {
     __shared__ int g[17];
     const int b = blockIdx.x;
-    const int t = threadIdx.x;
-    if (t <= a.k) {
-        const float2* st = a.stats + ((int64_t)b * (a.k + 1) + t) * a.nchunk;
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    // wave wv merges positions wv, wv+4, ...; lanes stride over the chunks
+    for (int pos = wv; pos <= a.k; pos += 4) {
+        const float2* st = a.stats + ((int64_t)b * (a.k + 1) + pos) * a.nchunk;
         float bv = -INFINITY;
         int bi = 0x7fffffff;
-        for (int64_t c = 0; c < a.nchunk; ++c) {
+        for (int64_t c = lane; c < a.nchunk; c += 64) {
             const float2 p = st[c];
             const int pi = __float_as_int(p.y);
             if (better(p.x, pi, bv, bi)) { bv = p.x; bi = pi; }
         }
-        g[t] = bi;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const float ov = __shfl_xor(bv, o, 64);
+            const int oi = __shfl_xor(bi, o, 64);
+            if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+        }
+        if (lane == 0) g[pos] = bi;
     }
     __syncthreads();
-    if (t == 0) {
+    if (t <= a.k) {
+        // a_b = number of leading drafts equal to the target argmax
+        int acc = a.k;
+        for (int i = 0; i < a.k; ++i)
+            if (a.x[(int64_t)b * a.k + i] != g[i]) { acc = i; break; }
         int32_t* out = a.out + (int64_t)b * (a.k + 1);
-        int acc = 0;
-        while (acc < a.k && a.x[(int64_t)b * a.k + acc] == g[acc]) {
-            out[acc] = g[acc];
-            ++acc;
-        }
-        out[acc] = g[acc];
-        for (int i = acc + 1; i <= a.k; ++i) out[i] = -1;
-        a.num[b] = acc;
+        out[t] = t < acc ? g[t] : (t == acc ? g[acc] : -1);
+        if (t == 0) a.num[b] = acc;
     }
 }
 
@@ -148,34 +161,40 @@ __global__ __launch_bounds__(kAThreads) void stoch_stats_kernel(AcceptArgs a) {
     if (c == 0 && r == 0 && threadIdx.x == 0) a.ctr[b] = 0u;   // ticket for stoch_sample_kernel
     const int64_t e0 = c * a.chunk;
     const int64_t e1 = min(e0 + a.chunk, a.V);
-    float t2[kPerThread];
-    float m = -INFINITY;
+    // Every thread streams its 8-element vectors and keeps an online
+    // (max m, sum 2^(t - m)) pair; the loads of all vectors are issued first.
+    uint4 raw[kPerThread / 8];
 #pragma unroll
     for (int j = 0; j < kPerThread / 8; ++j) {
         const int64_t e = e0 + ((int64_t)j * kAThreads + threadIdx.x) * 8;
-        float v[8];
+        if (VEC && e < e1) raw[j] = *reinterpret_cast<const uint4*>(z + e);
+    }
+    float m = -INFINITY, sum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kPerThread / 8; ++j) {
+        const int64_t e = e0 + ((int64_t)j * kAThreads + threadIdx.x) * 8;
         if (e < e1) {
-            load8<VEC>(z, e, a.V, v, 0.0f);
+            float v[8];
+            if (VEC) unpack8(raw[j], v);
+            else load8<false>(z, e, a.V, v, 0.0f);
+            float vm = -INFINITY;
 #pragma unroll
-            for (int q = 0; q < 8; ++q) v[q] = (e + q < e1) ? v[q] * a.c2 : -INFINITY;
-        } else {
+            for (int q = 0; q < 8; ++q) {
+                v[q] = (e + q < e1) ? v[q] * a.c2 : -INFINITY;
+                vm = fmaxf(vm, v[q]);
+            }
+            if (vm > m) {
+                sum = (m == -INFINITY) ? 0.0f : sum * exp2f(m - vm);
+                m = vm;
+            }
 #pragma unroll
-            for (int q = 0; q < 8; ++q) v[q] = -INFINITY;
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            t2[j * 8 + q] = v[q];
-            m = fmaxf(m, v[q]);
+            for (int q = 0; q < 8; ++q) sum += exp2f(v[q] - m);
         }
     }
-    m = block_max(m, red);
-    float s = 0.0f;
-    if (m != -INFINITY) {
-#pragma unroll
-        for (int q = 0; q < kPerThread; ++q) s += exp2f(t2[q] - m);
-    }
+    const float M = block_max(m, red);
+    float s = (m == -INFINITY) ? 0.0f : sum * exp2f(m - M);
     s = block_sum(s, red);
-    if (threadIdx.x == 0) a.stats[((int64_t)b * a.R + r) * a.nchunk + c] = make_float2(m, s);
+    if (threadIdx.x == 0) a.stats[((int64_t)b * a.R + r) * a.nchunk + c] = make_float2(M, s);
 }
 
 // Residual (or bonus) probability of element e given the sampled position.
@@ -209,51 +228,71 @@ __device__ __forceinline__ void dist8(const Dist& d, float c2, int64_t e, int64_
     }
 }
 
+// Online merge of (max, sum 2^(t - max)) pairs.
+__device__ __forceinline__ void merge_ms(float& m, float& z, float om, float oz) {
+    if (om == -INFINITY) return;
+    if (om > m) {
+        z = (m == -INFINITY ? 0.0f : z * exp2f(m - om)) + oz;
+        m = om;
+    } else {
+        z += oz * exp2f(om - m);
+    }
+}
+
 template <bool VEC>
 __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     __shared__ float sM[33], sZ[33];
-    __shared__ int s_j, s_last;
+    __shared__ int s_acc[16];
+    __shared__ int s_j, s_last, s_fallback, s_cstar;
     __shared__ float red[16];
     __shared__ double dsum[kAThreads / 64];
-    __shared__ int s_tok;
+    __shared__ double s_base, s_target;
+    __shared__ float s_mass[kMaxChunks];
+    __shared__ int s_found, s_lastnz;
     const int64_t c = blockIdx.x;
     const int b = blockIdx.y;
     const int t = threadIdx.x;
+    const int lane = t & 63, wv = t >> 6;
     const int k = a.k;
 
-    // 1. merge chunk statistics of every row of sequence b (fixed chunk order)
-    if (t < a.R) {
-        const float2* st = a.stats + ((int64_t)b * a.R + t) * a.nchunk;
-        float M = -INFINITY;
-        for (int64_t q = 0; q < a.nchunk; ++q) M = fmaxf(M, st[q].x);
-        float Z = 0.0f;
-        if (M != -INFINITY)
-            for (int64_t q = 0; q < a.nchunk; ++q)
-                if (st[q].x != -INFINITY) Z += st[q].y * exp2f(st[q].x - M);
-        sM[t] = M;
-        sZ[t] = Z;
+    // 1. merge the chunk statistics of every row of sequence b: wave wv takes
+    //    rows wv, wv+4, ...; lanes stride over chunks; fixed shuffle tree.
+    for (int r = wv; r < a.R; r += kAThreads / 64) {
+        const float2* st = a.stats + ((int64_t)b * a.R + r) * a.nchunk;
+        float m = -INFINITY, z = 0.0f;
+        for (int64_t q = lane; q < a.nchunk; q += 64) {
+            const float2 v = st[q];
+            merge_ms(m, z, v.x, v.y);
+        }
+        const float M = wave_max(m);
+        const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));
+        if (lane == 0) { sM[r] = M; sZ[r] = Z; }
     }
     __syncthreads();
 
-    // 2. sequential accept/reject (identical in every block of sequence b)
+    // 2. accept tests of the k drafts, evaluated in parallel (identical in
+    //    every block of sequence b); the first rejection j is then a scan.
+    if (t < k) {
+        const int32_t xi = a.x[(int64_t)b * k + t];
+        double p = 0.0, q = 0.0;
+        if (xi >= 0 && xi < a.V) {
+            const float zt = bf16_to_f32(a.zt[((int64_t)b * (k + 1) + t) * a.V + xi]);
+            p = exp2((double)(zt * a.c2) - (double)sM[t]) / (double)sZ[t];
+            if (a.zd) {
+                const float zd = bf16_to_f32(a.zd[((int64_t)b * k + t) * a.V + xi]);
+                q = exp2((double)(zd * a.c2) - (double)sM[k + 1 + t]) / (double)sZ[k + 1 + t];
+            } else {
+                q = 1.0;
+            }
+        }
+        const double ui = (double)a.u[(int64_t)b * (k + 1) + t];
+        s_acc[t] = (ui * q < p) ? 1 : 0;
+    }
+    __syncthreads();
     if (t == 0) {
         int j = k;
-        for (int i = 0; i < k; ++i) {
-            const int32_t xi = a.x[(int64_t)b * k + i];
-            double p = 0.0, q = 0.0;
-            if (xi >= 0 && xi < a.V) {
-                const float zt = bf16_to_f32(a.zt[((int64_t)b * (k + 1) + i) * a.V + xi]);
-                p = exp2((double)(zt * a.c2) - (double)sM[i]) / (double)sZ[i];
-                if (a.zd) {
-                    const float zd = bf16_to_f32(a.zd[((int64_t)b * k + i) * a.V + xi]);
-                    q = exp2((double)(zd * a.c2) - (double)sM[k + 1 + i]) / (double)sZ[k + 1 + i];
-                } else {
-                    q = 1.0;
-                }
-            }
-            const double ui = (double)a.u[(int64_t)b * (k + 1) + i];
-            if (!(ui * q < p)) { j = i; break; }
-        }
+        for (int i = 0; i < k; ++i)
+            if (!s_acc[i]) { j = i; break; }
         s_j = j;
     }
     __syncthreads();
@@ -302,105 +341,137 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     if (!s_last) return;
     __threadfence();
 
-    // 4. last block of sequence b: find the chunk holding u*R, then scan it.
-    //    If the residual vanished through rounding, sample from p_j instead.
-    if (t == 0) {
+    // 4. last block of sequence b: gather the chunk masses (if the residual
+    //    vanished through rounding, the chunk masses of p_j instead), find the
+    //    chunk holding u*R, then scan that chunk in vocabulary order.
+    {
         const float* ms = a.mass + (int64_t)b * a.nchunk;
-        double R = 0.0;
-        for (int64_t q = 0; q < a.nchunk; ++q)
-            R += (double)__hip_atomic_load(ms + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_tok = 0;
-        if (!(R > 0.0)) s_tok = 1;
+        float mine = 0.0f;
+        for (int64_t q = t; q < a.nchunk; q += kAThreads) {
+            const float v = __hip_atomic_load(ms + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_mass[q] = v;
+            mine += v;
+        }
+        const float R = block_sum(mine, red);
+        if (t == 0) s_fallback = !(R > 0.0f);
     }
     __syncthreads();
-    if (s_tok) {
+    if (s_fallback) {
+        const float2* st = a.stats + ((int64_t)b * a.R + j) * a.nchunk;
+        for (int64_t q = t; q < a.nchunk; q += kAThreads) {
+            const float2 v = st[q];
+            s_mass[q] = v.x == -INFINITY ? 0.0f : v.y * exp2f(v.x - d.mt) * d.inv_zt;
+        }
         d.zd_row = nullptr;
         d.skip = -1;
+        __syncthreads();
     }
-    // chunk masses (recomputed from stats for the fallback distribution p_j)
-    __shared__ int s_cstar;
-    __shared__ double s_base, s_target;
-    if (t == 0) {
-        const float* ms = a.mass + (int64_t)b * a.nchunk;
-        const float2* st = a.stats + ((int64_t)b * a.R + j) * a.nchunk;
-        double R = 0.0;
-        for (int64_t q = 0; q < a.nchunk; ++q) {
-            const double mq = s_tok ? (st[q].x == -INFINITY ? 0.0 : (double)st[q].y * exp2((double)(st[q].x - d.mt)) / (double)sZ[j])
-                                    : (double)__hip_atomic_load(ms + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            R += mq;
+    if (wv == 0) {
+        // wave 0: prefix over chunk masses in double (lane l owns a contiguous run)
+        const int64_t per = (a.nchunk + 63) / 64;
+        const int64_t q0 = lane * per, q1 = min(q0 + per, a.nchunk);
+        double loc = 0.0;
+        int64_t lastpos = -1;
+        for (int64_t q = q0; q < q1; ++q) {
+            loc += (double)s_mass[q];
+            if (s_mass[q] > 0.0f) lastpos = q;
         }
+        double incl = loc;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const double y = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += y;
+        }
+        const double R = __shfl(incl, 63, 64);
         const double target = (double)a.u[(int64_t)b * (k + 1) + k] * R;
-        double cum = 0.0;
+        double cum = incl - loc;
         int64_t cstar = -1;
-        int64_t last_pos = 0;
         double base = 0.0;
-        for (int64_t q = 0; q < a.nchunk; ++q) {
-            const double mq = s_tok ? (st[q].x == -INFINITY ? 0.0 : (double)st[q].y * exp2((double)(st[q].x - d.mt)) / (double)sZ[j])
-                                    : (double)__hip_atomic_load(ms + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (mq > 0.0) last_pos = q;
+        for (int64_t q = q0; q < q1; ++q) {
+            const double mq = (double)s_mass[q];
             if (cstar < 0 && cum + mq > target) { cstar = q; base = cum; }
             cum += mq;
         }
-        if (cstar < 0) { cstar = last_pos; base = cum; }   // u*R beyond the total (rounding)
-        s_cstar = (int)cstar;
-        s_base = base;
-        s_target = target;
+        // the first lane (in vocabulary order) that found the crossing wins
+        unsigned long long hit = __ballot(cstar >= 0);
+        int64_t lastall = lastpos;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const int64_t y = __shfl_xor(lastall, o, 64);
+            lastall = y > lastall ? y : lastall;
+        }
+        if (hit) {
+            const int src = __ffsll((long long)hit) - 1;
+            const int64_t cs = __shfl(cstar, src, 64);
+            const double bs = __shfl(base, src, 64);
+            if (lane == 0) { s_cstar = (int)cs; s_base = bs; }
+        } else if (lane == 0) {
+            s_cstar = (int)(lastall >= 0 ? lastall : 0);   // u*R beyond the total (rounding)
+            s_base = R;
+        }
+        if (lane == 0) s_target = target;
     }
+    if (t == 0) { s_found = 0x7fffffff; s_lastnz = -1; }
     __syncthreads();
     const int64_t cs = s_cstar;
     const double tgt = s_target - s_base;
     const int64_t f0 = cs * a.chunk;
     const int64_t f1 = min(f0 + a.chunk, a.V);
-    // contiguous ownership: thread t scans elements [f0 + 32t, f0 + 32t + 32)
-    float r[kPerThread];
+    // contiguous ownership: thread t scans elements [f0 + 128t, f0 + 128t + 128).
+    // Pass 1: per-thread sums; exclusive scan across the block; pass 2: the
+    // thread whose range holds the crossing walks its elements again.
     double mine = 0.0;
-#pragma unroll
+    int lastnz = -1;
+#pragma unroll 4
     for (int jj = 0; jj < kPerThread / 8; ++jj) {
         const int64_t e = f0 + (int64_t)t * kPerThread + jj * 8;
         if (e < f1) {
-            dist8<VEC>(d, a.c2, e, f1, a.V, r + jj * 8);
-        } else {
+            float r[8];
+            dist8<VEC>(d, a.c2, e, f1, a.V, r);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) r[jj * 8 + q] = 0.0f;
+            for (int q = 0; q < 8; ++q) {
+                mine += (double)r[q];
+                if (r[q] > 0.0f) lastnz = (int)(e + q);
+            }
         }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) mine += (double)r[jj * 8 + q];
     }
-    // exclusive scan of the per-thread sums (wave scan, then across waves)
-    const int lane = t & 63, w = t >> 6;
     double incl = mine;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
         const double y = __shfl_up(incl, o, 64);
         if (lane >= o) incl += y;
     }
-    if (lane == 63) dsum[w] = incl;
-    __shared__ int s_found, s_lastnz;
-    if (t == 0) { s_found = 0x7fffffff; s_lastnz = -1; }
+    if (lane == 63) dsum[wv] = incl;
     __syncthreads();
     double before = 0.0;
-    for (int q = 0; q < w; ++q) before += dsum[q];
+    for (int q = 0; q < wv; ++q) before += dsum[q];
     double cum = before + incl - mine;
-    int found = -1, lastnz = -1;
-#pragma unroll
-    for (int q = 0; q < kPerThread; ++q) {
-        const int64_t e = f0 + (int64_t)t * kPerThread + q;
-        if (r[q] > 0.0f) lastnz = (int)e;
-        cum += (double)r[q];
-        if (found < 0 && e < f1 && cum > tgt) found = (int)e;
+    int found = -1;
+    if (cum <= tgt && cum + mine > tgt) {
+        for (int jj = 0; jj < kPerThread / 8 && found < 0; ++jj) {
+            const int64_t e = f0 + (int64_t)t * kPerThread + jj * 8;
+            if (e < f1) {
+                float r[8];
+                dist8<VEC>(d, a.c2, e, f1, a.V, r);
+                for (int q = 0; q < 8; ++q) {
+                    cum += (double)r[q];
+                    if (found < 0 && e + q < f1 && cum > tgt) found = (int)(e + q);
+                }
+            }
+        }
     }
     if (found >= 0) atomicMin(&s_found, found);
     if (lastnz >= 0) atomicMax(&s_lastnz, lastnz);
     __syncthreads();
-    if (t == 0) {
+    if (t <= k) {
         int tok = s_found;
         if (tok == 0x7fffffff) tok = s_lastnz >= 0 ? s_lastnz : (int)f0;
         int32_t* out = a.out + (int64_t)b * (k + 1);
-        for (int i = 0; i < j; ++i) out[i] = a.x[(int64_t)b * k + i];
-        out[j] = tok;
-        for (int i = j + 1; i <= k; ++i) out[i] = -1;
-        a.num[b] = j;
-        a.ctr[b] = 0u;
+        out[t] = t < j ? a.x[(int64_t)b * k + t] : (t == j ? tok : -1);
+        if (t == 0) {
+            a.num[b] = j;
+            a.ctr[b] = 0u;
+        }
     }
 }
 
@@ -440,7 +511,7 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
         else hipLaunchKernelGGL(greedy_partial_kernel<false>, g1, dim3(kAThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(greedy_final_kernel, dim3((unsigned)B), dim3(64), 0, stream, a);
+        hipLaunchKernelGGL(greedy_final_kernel, dim3((unsigned)B), dim3(256), 0, stream, a);
         return hipGetLastError();
     }
     a.R = (int)((k + 1) + (zd ? k : 0));

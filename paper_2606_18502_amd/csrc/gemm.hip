@@ -81,19 +81,26 @@ struct GemmCfg {
     static constexpr int kLdsBytes = STAGES * kStageBytes;
     static_assert(kRows % 16 == 0, "tile rows must be multiples of 16");
     static_assert(kGroups % kWaves == 0, "every wave issues the same number of loads per stage");
-    static_assert((STAGES - 2) * kGroupsPerWave < 64, "vmcnt range");
+    static_assert((STAGES - 1) * kGroupsPerWave < 64, "vmcnt range");
 };
+
+// LDS swizzle.  gfx950's LDS has 64 banks of 4 bytes (256 bytes per cycle),
+// so a ds_read_b128 serves 16 lanes per cycle.  Rows are 128 bytes, so rows
+// r and r^1 share a 256-byte bank line; placing logical chunk c of row r in
+// slot c ^ ((r >> 1) & 7) gives the 16 lanes that read one logical chunk of
+// 16 consecutive rows 16 different 16-byte bank groups.
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
 template <class C>
 __device__ __forceinline__ void issue_stage(const GemmArgs& g, char* stage, int m0, int n0,
                                             int64_t kbyte, int wave, int lane) {
     const int r_in = lane >> 3;       // row within the 8-row group
     const int slot = lane & 7;        // LDS slot this lane fills
-    const int chunk = slot ^ r_in;    // logical 16-byte chunk loaded into it
 #pragma unroll
     for (int i = 0; i < C::kGroupsPerWave; ++i) {
         const int grp = wave + i * C::kWaves;
         const int row = grp * 8 + r_in;
+        const int chunk = slot ^ swz(row);   // logical 16-byte chunk loaded into it
         const uint8_t* src;
         if (row < C::BM) {
             int m = m0 + row;
@@ -125,59 +132,105 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // `row`, each in its swizzled slot.  The LDS reads are issued as inline asm so
 // that the compiler does not treat them as readers of the direct-to-LDS loads
 // still in flight for other stages (it would drain them all); completion is
-// awaited explicitly by frag_wait().
+// awaited explicitly.
+__device__ __forceinline__ u32x4 lds_half(uint32_t stage, int row, int chunk) {
+    const uint32_t a = stage + (uint32_t)row * kBK + ((uint32_t)(chunk ^ swz(row)) << 4);
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+
 __device__ __forceinline__ v8i lds_frag(uint32_t stage, int row, int kg) {
-    const int sw = row & 7;
-    const uint32_t base = stage + (uint32_t)row * kBK;
-    const uint32_t a0 = base + ((uint32_t)((2 * kg) ^ sw) << 4);
-    const uint32_t a1 = base + ((uint32_t)((2 * kg + 1) ^ sw) << 4);
-    u32x4 lo, hi;
-    asm volatile("ds_read_b128 %0, %1" : "=v"(lo) : "v"(a0));
-    asm volatile("ds_read_b128 %0, %1" : "=v"(hi) : "v"(a1));
+    const u32x4 lo = lds_half(stage, row, 2 * kg);
+    const u32x4 hi = lds_half(stage, row, 2 * kg + 1);
     v8i r;
     r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
     r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
     return r;
 }
 
-// Wait for every outstanding LDS read; each fragment passes through an empty
-// asm after the wait, so no use of it can be scheduled before the wait.
+// Wait until at most N LDS reads are outstanding (they complete in order);
+// the fragment passes through an empty asm after the wait, so no use of it
+// can be scheduled before the wait.
 template <int N>
-__device__ __forceinline__ void frag_wait(v8i (&f)[N]) {
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-#pragma unroll
-    for (int i = 0; i < N; ++i) asm volatile("" : "+v"(f[i]));
+__device__ __forceinline__ void frag_ready(v8i& f) {
+    static_assert(N >= 0 && N < 16, "lgkmcnt range");
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+    asm volatile("" : "+v"(f));
 }
 
-// One K-step on compile-time stage S: wait for its loads, barrier, refill the
-// stage consumed one step earlier, multiply.  Every stage is its own LDS
-// object and every wait count is a compile-time constant, so the compiler can
-// tell that the direct-to-LDS loads still in flight target other stages and
-// does not drain them before the LDS reads of this one.  Past the end of the
-// K range the refill re-loads the last K-step (in bounds, never multiplied),
-// which keeps the number of loads in flight -- and so the wait -- uniform.
-template <class C, int STAGES, int WTM, int WTN, int S>
-__device__ __forceinline__ void kstep(const GemmArgs& g, char* const* stages, int it, int nk, int ks0, int m0,
-                                      int n0, int wave, int lane, int wm, int wn, v4f (&acc)[WTN][WTM]) {
-    wait_vmcnt<(STAGES - 2) * C::kGroupsPerWave>();
-    __builtin_amdgcn_s_barrier();
-    const int nxt = min(it + STAGES - 1, nk - 1);
-    issue_stage<C>(g, stages[(S + STAGES - 1) % STAGES], m0, n0, (int64_t)(ks0 + nxt) * kBK, wave, lane);
-    const uint32_t st = lds_addr(stages[S]);
+// Operand fragments of one K-step held in registers: WTM activation blocks
+// and WTN weight blocks.
+template <int WTM, int WTN>
+struct Frags {
+    v8i a[WTM];
+    v8i w[WTN];
+};
+
+template <class C, int WTM, int WTN>
+__device__ __forceinline__ void read_frags(Frags<WTM, WTN>& f, uint32_t st, int wm, int wn, int lane) {
     const int kg = lane >> 4;
     const int r16 = lane & 15;
-    v8i frag[WTM + WTN];
 #pragma unroll
-    for (int j = 0; j < WTM; ++j) frag[j] = lds_frag(st, (wm * WTM + j) * 16 + r16, kg);
+    for (int j = 0; j < WTM; ++j) f.a[j] = lds_frag(st, (wm * WTM + j) * 16 + r16, kg);
 #pragma unroll
-    for (int i = 0; i < WTN; ++i) frag[WTM + i] = lds_frag(st, C::BM + (wn * WTN + i) * 16 + r16, kg);
-    frag_wait(frag);
+    for (int i = 0; i < WTN; ++i) f.w[i] = lds_frag(st, C::BM + (wn * WTN + i) * 16 + r16, kg);
+}
+
+__device__ __forceinline__ void lds_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// One K-step `it` on compile-time stage S with fragments `cur` (already read):
+//   1. wait until the loads of step it+1 have landed (this wave), barrier (all waves);
+//   2. refill stage S -- its data is already in `cur` in every wave -- with step it+STAGES;
+//   3. issue the LDS reads of step it+1 into `nxt` while the MFMAs of step it run.
+// Every stage is its own LDS object and every wait count is a compile-time
+// constant, so the compiler does not drain the direct-to-LDS loads of other
+// stages; past the end of the K range the refill re-loads the last K-step (in
+// bounds, never multiplied), which keeps the number of loads in flight -- and
+// so the wait -- uniform.
+template <class C, int STAGES, int WTM, int WTN, int S>
+__device__ __forceinline__ void kstep(const GemmArgs& g, char* const* stages, int it, int nk, int ks0, int krot,
+                                      int m0, int n0, int wave, int lane, int wm, int wn, v4f (&acc)[WTN][WTM],
+                                      Frags<WTM, WTN>& cur, Frags<WTM, WTN>& nxt) {
+    wait_vmcnt<(STAGES - 2) * C::kGroupsPerWave>();
+    __builtin_amdgcn_s_barrier();
+    const int refill = min(it + STAGES, nk - 1);
+    issue_stage<C>(g, stages[S], m0, n0, (int64_t)(ks0 + (refill + krot) % nk) * kBK, wave, lane);
+    // MFMAs of step it, with the LDS reads of step it+1 spread between them so
+    // the LDS command queue never fills and blocks MFMA issue.  Each group is
+    // fenced with sched_barrier to keep this order.  On the last step the
+    // reads target the current stage (in bounds, results unused), which keeps
+    // the sequence free of branches.
+    const bool more = it + 1 < nk;
+    const uint32_t st_next = lds_addr(stages[more ? (S + 1) % STAGES : S]);
+    const int kg = lane >> 4;
+    const int r16 = lane & 15;
+    constexpr int kMfma = WTM * WTN;
+    constexpr int kReads = 2 * (WTM + WTN);
 #pragma unroll
-    for (int i = 0; i < WTN; ++i)
+    for (int t = 0; t < kMfma; ++t) {
+        const int i = t / WTM, j = t % WTM;
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(cur.w[i], cur.a[j], acc[i][j], 0, 0, 0, 0, 0, 0);
 #pragma unroll
-        for (int j = 0; j < WTM; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(frag[WTM + i], frag[j], acc[i][j], 0, 0,
-                                                                         0, 0, 0, 0);
+        for (int r = 0; r < kReads; ++r) {
+            if ((r * kMfma) / kReads == t) {
+                const int f = r / 2, h = r & 1;
+                const int row = f < WTM ? (wm * WTM + f) * 16 + r16 : C::BM + (wn * WTN + f - WTM) * 16 + r16;
+                const u32x4 v = lds_half(st_next, row, 2 * kg + h);
+                v8i& dst = f < WTM ? nxt.a[f] : nxt.w[f - WTM];
+                dst[4 * h + 0] = v[0];
+                dst[4 * h + 1] = v[1];
+                dst[4 * h + 2] = v[2];
+                dst[4 * h + 3] = v[3];
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    lds_wait_all();
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) asm volatile("" : "+v"(nxt.a[j]));
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) asm volatile("" : "+v"(nxt.w[i]));
 }
 
 template <int WTM, int WTN, int WM, int WN, int STAGES>
@@ -210,6 +263,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     const int ks0 = split * ks_per;
     const int ks1 = min(g.ksteps, ks0 + ks_per);
     const int nk = ks1 - ks0;
+    // Workgroups that share an activation tile walk K from different
+    // starting points, so they do not all request the same bytes at once.
+    const int krot = (nt * 7 + split) % nk;
 
     v4f acc[WTN][WTM];
 #pragma unroll
@@ -217,45 +273,88 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < WTM; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    // prologue: STAGES-1 stages in flight
+    // prologue: all STAGES stages in flight, then the fragments of step 0
 #pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
-        issue_stage<C>(g, stages[s], m0, n0, (int64_t)(ks0 + min(s, nk - 1)) * kBK, wave, lane);
-
-    for (int base = 0; base < nk; base += STAGES) {
-        kstep<C, STAGES, WTM, WTN, 0>(g, stages, base, nk, ks0, m0, n0, wave, lane, wm, wn, acc);
-        if (base + 1 < nk) kstep<C, STAGES, WTM, WTN, 1>(g, stages, base + 1, nk, ks0, m0, n0, wave, lane, wm, wn, acc);
-        if constexpr (STAGES > 2)
-            if (base + 2 < nk) kstep<C, STAGES, WTM, WTN, 2>(g, stages, base + 2, nk, ks0, m0, n0, wave, lane, wm, wn, acc);
-        if constexpr (STAGES > 3)
-            if (base + 3 < nk) kstep<C, STAGES, WTM, WTN, 3>(g, stages, base + 3, nk, ks0, m0, n0, wave, lane, wm, wn, acc);
+    for (int s = 0; s < STAGES; ++s)
+        issue_stage<C>(g, stages[s], m0, n0, (int64_t)(ks0 + (min(s, nk - 1) + krot) % nk) * kBK, wave, lane);
+    // The epilogue's scales, fetched now so their latency hides behind the
+    // main loop (rows and columns past the edge read a valid neighbour).
+    float sa_reg[WTM];
+    float sw_reg[WTN][4];
+    {
+        const int kg0 = lane >> 4, r0 = lane & 15;
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) {
+            const int m = min(m0 + (wm * WTM + j) * 16 + r0, g.M - 1);
+            sa_reg[j] = g.a_per_tensor ? g.sa[0] : g.sa[m];
+        }
+#pragma unroll
+        for (int i = 0; i < WTN; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int n = min(n0 + (wn * WTN + i) * 16 + 4 * kg0 + r, g.N - 1);
+                sw_reg[i][r] = g.w_per_tensor ? g.sw[0] : g.sw[n];
+            }
     }
+    Frags<WTM, WTN> f0, f1;
+    wait_vmcnt<(STAGES - 1) * C::kGroupsPerWave>();
+    __builtin_amdgcn_s_barrier();
+    read_frags<C>(f0, lds_addr(stages[0]), wm, wn, lane);
+    lds_wait_all();
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) asm volatile("" : "+v"(f0.a[j]));
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) asm volatile("" : "+v"(f0.w[i]));
+
+    // the loop body covers lcm(STAGES, 2) steps so that both the stage and the
+    // register set of every step are compile-time constants
+#define SPEC_STEP(S, CUR, NXT)                                                                              \
+    if (base + (S) < nk)                                                                                    \
+        kstep<C, STAGES, WTM, WTN, (S) % STAGES>(g, stages, base + (S), nk, ks0, krot, m0, n0, wave, lane, wm, \
+                                                 wn, acc, CUR, NXT);
+    constexpr int U = (STAGES % 2 == 0) ? STAGES : 2 * STAGES;
+    for (int base = 0; base < nk; base += U) {
+        SPEC_STEP(0, f0, f1)
+        SPEC_STEP(1, f1, f0)
+        if constexpr (U > 2) {
+            SPEC_STEP(2, f0, f1)
+            SPEC_STEP(3, f1, f0)
+        }
+        if constexpr (U > 4) {
+            SPEC_STEP(4, f0, f1)
+            SPEC_STEP(5, f1, f0)
+        }
+        if constexpr (U > 6) {
+            SPEC_STEP(6, f0, f1)
+            SPEC_STEP(7, f1, f0)
+        }
+    }
+#undef SPEC_STEP
     wait_vmcnt<0>();   // no direct-to-LDS write may outlive the workgroup
 
     const int kg = lane >> 4;
     const int r16 = lane & 15;
-    // epilogue: lane holds D[n = 4*(lane/16) + r][m = lane%16] of each 16x16 block
+    // epilogue: lane holds D[n = 4*(lane/16) + r][m = lane%16] of each 16x16
+    // block; the scales were fetched into registers before the main loop.
 #pragma unroll
     for (int i = 0; i < WTN; ++i) {
         const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
-        if (n >= g.N) continue;
 #pragma unroll
         for (int j = 0; j < WTM; ++j) {
             const int m = m0 + (wm * WTM + j) * 16 + r16;
-            if (m >= g.M) continue;
             const v4f a = acc[i][j];
+            const bool ok = (n < g.N) && (m < g.M);
             if (g.splits > 1) {
-                float* dst = g.partial + ((int64_t)split * g.M + m) * g.ldp + n;
-                *reinterpret_cast<float4*>(dst) = make_float4(a[0], a[1], a[2], a[3]);
+                if (ok) {
+                    float* dst = g.partial + ((int64_t)split * g.M + m) * g.ldp + n;
+                    *reinterpret_cast<float4*>(dst) = make_float4(a[0], a[1], a[2], a[3]);
+                }
                 continue;
             }
-            const float sa = g.a_per_tensor ? g.sa[0] : g.sa[m];
             float y[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float sw = g.w_per_tensor ? g.sw[0] : g.sw[n + r < g.N ? n + r : g.N - 1];
-                y[r] = (a[r] * sa) * sw;
-            }
+            for (int r = 0; r < 4; ++r) y[r] = (a[r] * sa_reg[j]) * sw_reg[i][r];
+            if (!ok) continue;
             if (g.out_f32) {
                 float* dst = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
                 if (n + 3 < g.N) {
@@ -319,22 +418,22 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g) {
 }
 
 // ---- tile configurations -------------------------------------------------
-// kind  BM x BN   waves (wave tile)     stages  LDS
-//  0    64 x 64   2x2 (32x32)           4       64 KiB   small M
+// kind  BM x BN   waves (wave tile)     stages  LDS      used for
+//  0    64 x 64   2x2 (32x32)           4       64 KiB   M <= 64
 //  1    80 x 128  1x2 (80x64)           4       104 KiB  M <= 80
-//  2   320 x 128  4x2 (80x64)           2       112 KiB
+//  2   160 x 224  2x2 (80x112)          3       144 KiB  M <= 320, N % 224 == 0
 //  3   256 x 128  2x2 (128x64)          3       144 KiB  large M
-//  4   320 x 64   4x2 (80x32)           3       144 KiB
-//  5   160 x 128  2x2 (80x64)           4       144 KiB
-//  6   320 x 32   4x1 (80x32)           3       132 KiB
+//  4   160 x 192  2x2 (80x96)           3       132 KiB  M <= 320, N % 192 == 0
+//  5   160 x 128  2x2 (80x64)           4       144 KiB  M <= 320
+//  6   320 x 64   4x1 (80x64)           3       144 KiB
 //  7   160 x 64   2x2 (80x32)           4       112 KiB
 using Cfg0 = GemmCfg<2, 2, 2, 2, 4>;
 using Cfg1 = GemmCfg<5, 4, 1, 2, 4>;
-using Cfg2 = GemmCfg<5, 4, 4, 2, 2>;
+using Cfg2 = GemmCfg<5, 7, 2, 2, 3>;
 using Cfg3 = GemmCfg<8, 4, 2, 2, 3>;
-using Cfg4 = GemmCfg<5, 2, 4, 2, 3>;
+using Cfg4 = GemmCfg<5, 6, 2, 2, 3>;
 using Cfg5 = GemmCfg<5, 4, 2, 2, 4>;
-using Cfg6 = GemmCfg<5, 2, 4, 1, 3>;
+using Cfg6 = GemmCfg<5, 4, 4, 1, 3>;
 using Cfg7 = GemmCfg<5, 2, 2, 2, 4>;
 
 constexpr int kCfgBM[8] = {Cfg0::BM, Cfg1::BM, Cfg2::BM, Cfg3::BM, Cfg4::BM, Cfg5::BM, Cfg6::BM, Cfg7::BM};
@@ -354,8 +453,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
     GemmPlan p{};
     if (M <= 64) p.kind = 0;
     else if (M <= 80) p.kind = 1;
-    else if (M <= 160) p.kind = 5;
-    else if (M <= 640) p.kind = 2;
+    else if (M <= 320) p.kind = (N % 224 == 0 && N >= 224 * 64) ? 2 : (N % 192 == 0 ? 4 : 5);
     else p.kind = 3;
     const int ksteps = (int)(K / kBK);
     int splits = 0;
@@ -405,11 +503,11 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
     switch (p.kind) {
         case 0: e = launch_cfg<Cfg0, 2, 2, 2, 2, 4>(g, stream); break;
         case 1: e = launch_cfg<Cfg1, 5, 4, 1, 2, 4>(g, stream); break;
-        case 2: e = launch_cfg<Cfg2, 5, 4, 4, 2, 2>(g, stream); break;
+        case 2: e = launch_cfg<Cfg2, 5, 7, 2, 2, 3>(g, stream); break;
         case 3: e = launch_cfg<Cfg3, 8, 4, 2, 2, 3>(g, stream); break;
-        case 4: e = launch_cfg<Cfg4, 5, 2, 4, 2, 3>(g, stream); break;
+        case 4: e = launch_cfg<Cfg4, 5, 6, 2, 2, 3>(g, stream); break;
         case 5: e = launch_cfg<Cfg5, 5, 4, 2, 2, 4>(g, stream); break;
-        case 6: e = launch_cfg<Cfg6, 5, 2, 4, 1, 3>(g, stream); break;
+        case 6: e = launch_cfg<Cfg6, 5, 4, 4, 1, 3>(g, stream); break;
         default: e = launch_cfg<Cfg7, 5, 2, 2, 2, 4>(g, stream); break;
     }
     if (e != hipSuccess || p.splits == 1) return e;

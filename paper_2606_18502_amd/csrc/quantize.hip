@@ -8,7 +8,7 @@
 // derives the scale, and encodes the registers it already holds.  HBM traffic
 // is therefore the algorithmic 2 bytes in + 1 byte out per element (4 + 1 for
 // the SiLU-gated input) plus 4 bytes of scale per row.  Rows wider than
-// kMaxChunks*8*256 elements take a second pass that re-reads the row.
+// 16384 elements take a second pass that re-reads the row.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
