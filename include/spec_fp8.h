@@ -82,7 +82,10 @@ typedef enum {
  *
  * E4M3(.) rounds to nearest with ties to the even mantissa and saturates any
  * magnitude above 448 to +-448; NaN gives 0x7F; the sign of zero is kept.
- * fl32(a/b) is the correctly rounded fp32 quotient.  Results are bit-exact.
+ * fl32(a/b) is the correctly rounded fp32 quotient.  Results are bit-exact
+ * given v.  For SILU_MUL, silu(g) = g / (1 + e^-g) is evaluated in fp32 with
+ * the hardware exp2 and reciprocal (about 1 ulp each), so bf16(v) can differ
+ * from an exact evaluation by one bf16 ulp at near-ties of its rounding.
  *
  * x       bf16 [rows, ld_x]; cols (or 2*cols for SILU_MUL) <= ld_x.
  * scales  fp32 [rows] (PER_ROW, written) or fp32 [1] (PER_TENSOR, read; must be
@@ -154,7 +157,7 @@ spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, s
  * num_accepted  int32 [B]: a_b in [0, k]; a_b + 1 tokens are emitted.
  * workspace     >= spec_verify_accept_workspace_bytes(B, k, V) bytes; contents on
  *               entry are ignored.
- * Requirements: B >= 0 (0 is a no-op), 1 <= k <= 16, 1 <= V <= 2^23 and
+ * Requirements: B >= 0 (0 is a no-op), 1 <= k <= 16, 1 <= V <= 2^22 and
  * B*(2k+1) <= 65535 (SPEC_ERR_UNSUPPORTED otherwise);
  * temperature finite and >= 0 (SPEC_ERR_VALUE otherwise).  Probabilities are
  * computed in fp32; a decision within ~1e-5 relative of its boundary may

@@ -1,24 +1,29 @@
 // Acceptance test of the speculative-decoding verify step.
 //
 // Greedy (T == 0):
-//   greedy_partial_kernel  (chunk, row) -> max logit and its lowest index
+//   greedy_partial_kernel  (row, slice) items -> max logit and its lowest index
 //   greedy_final_kernel    b -> argmax per position, longest matching prefix
 // Speculative sampling (T > 0):
-//   stoch_stats_kernel     (chunk, row) -> chunk max m and sum 2^(t - m) of
-//                          t = z * log2(e)/T (the tempered logit in base 2),
-//                          for target rows 0..k and draft rows 0..k-1
-//   stoch_sample_kernel    (chunk, b)   -> every block merges the chunk
-//                          statistics of its sequence in chunk order, takes the
-//                          (identical) accept/reject decisions, and sums the
-//                          residual distribution over its chunk; the last block
-//                          of the sequence to finish (an atomic ticket) locates
-//                          the chunk holding u*R, scans that chunk in vocabulary
-//                          order and writes the tokens.
-// The vocabulary is split into chunks of 8192 so that B*(2k+1)*ceil(V/8192)
-// workgroups stream the logits once (2 bytes per element, 16-byte loads,
-// each wave reading 1 KiB contiguous per instruction).  All reductions use a
-// fixed order, so results are deterministic.  The sample kernel re-reads only
-// the row(s) of the position where sampling happens (<= 2 rows per sequence).
+//   stoch_stats_kernel     (row, slice) items -> slice max m and sum 2^(t - m) of
+//                          t = z * log2(e)/T (the tempered logit in base 2), for
+//                          target rows 0..k and draft rows 0..k-1
+//   stoch_sample_kernel    (chunk, b) -> every block merges the slice statistics
+//                          of its sequence in slice order, takes the (identical)
+//                          accept/reject decisions and sums the residual
+//                          distribution over its chunk; the last block of the
+//                          sequence to finish (an atomic ticket) locates the
+//                          chunk holding u*R, scans it in vocabulary order and
+//                          writes the tokens.
+//
+// The two streaming kernels run a persistent grid in which every WAVE walks
+// (row, slice) items of 4096 logits with the loads of its next item in flight
+// while it reduces the current one, so HBM sees one continuous stream of
+// 2 bytes per logit and no item needs a workgroup barrier.  Items are strided
+// over the waves, so at any moment the chip reads one contiguous stretch of
+// the logit tensors.  The sample kernel re-reads only the row(s) of the
+// position where sampling happens (<= 2 rows per sequence), with every load of
+// a thread issued before it computes.  All reductions use a fixed order, so
+// results are deterministic.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -27,9 +32,14 @@ namespace specfp8 {
 namespace {
 
 constexpr int kAThreads = 256;
-constexpr int kPerThread = 128;                       // elements per thread per chunk
-constexpr int64_t kChunk = kAThreads * kPerThread;    // 32768
-constexpr int kMaxChunks = 1024;                      // V <= 32M
+constexpr int kWavesPerBlock = kAThreads / kWave;
+constexpr int kVecs = 8;                               // 16-byte vectors per lane per item
+constexpr int64_t kSlice = (int64_t)kWave * kVecs * 8;         // 4096 logits per wave item
+constexpr int kPerThread = kVecs * 8;                  // 64 logits per thread (sample kernel)
+constexpr int64_t kChunk = (int64_t)kAThreads * kPerThread;   // 16384 logits per sample block
+constexpr int kMaxChunks = kAThreads;                 // V <= 2^22: one chunk per thread
+constexpr int kStreamWavesPerCU = 16;
+constexpr int kCUs = 256;
 
 struct AcceptArgs {
     const uint16_t* zt;
@@ -38,92 +48,154 @@ struct AcceptArgs {
     const float* u;
     int32_t* out;
     int32_t* num;
-    float2* stats;         // [B][R][nchunk]
-    float* mass;           // [B][nchunk]
+    float2* stats;         // [B][R][nslice]
+    double* chunkm;        // [B][nchunk] residual mass per chunk
+    double* finem;         // [B][nchunk][256] residual mass per 64-element range
     unsigned int* ctr;     // [B]
-    int64_t V, chunk, nchunk;
-    int B, k, R;           // R = rows per sequence in `stats`
+    int64_t V, nchunk;
+    uint32_t nslice, items;   // slices per row; rows * nslice (< 2^31)
+    int B, k;
+    uint32_t R;            // rows per sequence in `stats`
     float c2;              // log2(e) / T
 };
 
+using Raw = uint4[kVecs];
+
+// Slice layout: vector j of lane l starts at element e0 + (j * 64 + l) * 8, so
+// one load instruction of a wave reads 1 KiB contiguous.
+__device__ __forceinline__ int64_t slice_vec(int64_t e0, int j, int lane) {
+    return e0 + ((int64_t)j * kWave + lane) * 8;
+}
+
+// Issue the loads of one slice (vector path only).  Out-of-range vectors load
+// the last full vector of the slice instead (always in bounds, V % 8 == 0);
+// their values are masked where they are used.
 template <bool VEC>
-__device__ __forceinline__ void load8(const uint16_t* __restrict__ row, int64_t e, int64_t V, float out[8],
-                                      float fill) {
+__device__ __forceinline__ void load_slice(const uint16_t* __restrict__ row, int64_t e0, int64_t e1, int lane,
+                                           Raw& raw) {
+    if (!VEC) return;
+#pragma unroll
+    for (int j = 0; j < kVecs; ++j) {
+        const int64_t e = min(slice_vec(e0, j, lane), e1 - 8);
+        raw[j] = *reinterpret_cast<const uint4*>(row + e);
+    }
+}
+
+// Element e + q of a group of 8 starting at e < e1 exists.  With vector
+// loads, V and every range end are multiples of 8, so the whole group does.
+template <bool VEC>
+__device__ __forceinline__ bool in8(int64_t e, int q, int64_t e1) { return VEC || e + q < e1; }
+
+// 8 values starting at e (< e1): from the loaded vector, or element-wise when
+// V is not a multiple of 8 (no vector loads then).  Elements >= e1 read `fill`.
+template <bool VEC>
+__device__ __forceinline__ void vals8(const uint16_t* __restrict__ row, const uint4& raw, int64_t e, int64_t e1,
+                                      float fill, float out[8]) {
     if (VEC) {
-        const uint4 v = *reinterpret_cast<const uint4*>(row + e);
-        unpack8(v, out);
+        unpack8(raw, out);
     } else {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) out[i] = (e + i < V) ? bf16_to_f32(row[e + i]) : fill;
+        for (int q = 0; q < 8; ++q) out[q] = (e + q < e1) ? bf16_to_f32(row[e + q]) : fill;
+    }
+}
+
+// Number of stream waves: at most kStreamWavesPerCU per compute unit, with
+// the items spread so that every wave takes the same count (but the last).
+inline int64_t stream_waves(int64_t items) {
+    const int64_t cap = (int64_t)kCUs * kStreamWavesPerCU;
+    const int64_t per = (items + cap - 1) / cap;
+    return (items + per - 1) / per;
+}
+
+// Persistent wave loop over items it = gw, gw + GW, ...: the slice of item
+// it + GW is loaded while item it is reduced (two register buffers).
+template <bool VEC, class RowOf, class Body>
+__device__ __forceinline__ void stream_items(const AcceptArgs& a, RowOf row_of, Body body) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const uint32_t gw = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const uint32_t GW = gridDim.x * kWavesPerBlock;
+    auto lo = [&](uint32_t it) { return (int64_t)(it % a.nslice) * kSlice; };
+    auto hi = [&](uint32_t it) { return min(lo(it) + kSlice, a.V); };
+    auto clampi = [&](uint32_t it) { return it < a.items ? it : a.items - 1; };
+    if (gw >= a.items) return;
+    Raw r0, r1;
+    load_slice<VEC>(row_of(gw / a.nslice), lo(gw), hi(gw), lane, r0);
+    for (uint32_t it = gw; it < a.items; it += 2 * GW) {
+        const uint32_t n1 = clampi(it + GW), n2 = clampi(it + 2 * GW);
+        load_slice<VEC>(row_of(n1 / a.nslice), lo(n1), hi(n1), lane, r1);
+        body(it, r0);
+        load_slice<VEC>(row_of(n2 / a.nslice), lo(n2), hi(n2), lane, r0);
+        if (it + GW < a.items) body(it + GW, r1);
     }
 }
 
 // ------------------------------------------------------------------ greedy
 
-struct ValIdx {
-    float v;
-    int i;
-};
-
 __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
     return v > bv || (v == bv && i < bi);
 }
 
-template <bool VEC>
-__global__ __launch_bounds__(kAThreads) void greedy_partial_kernel(AcceptArgs a) {
-    __shared__ float sv[kAThreads / 64];
-    __shared__ int si[kAThreads / 64];
-    const int64_t c = blockIdx.x;
-    const int64_t row = blockIdx.y;                  // b*(k+1) + i
-    const uint16_t* z = a.zt + row * a.V;
-    const int64_t e0 = c * a.chunk;
-    const int64_t e1 = min(e0 + a.chunk, a.V);
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-    uint4 raw[kPerThread / 8];
+// Lane maximum of the logits of one slice (8-element groups, v_max3 pairs).
+// Missing elements (non-vector path past e1) read NaN, which fmaxf ignores.
+template <bool VEC, bool FULL>
+__device__ __forceinline__ float slice_max(const uint16_t* z, const Raw& raw, int64_t e0, int64_t e1, int lane) {
+    float zm = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < kPerThread / 8; ++j) {           // all loads in flight first
-        const int64_t e = e0 + ((int64_t)j * kAThreads + threadIdx.x) * 8;
-        if (VEC && e < e1) raw[j] = *reinterpret_cast<const uint4*>(z + e);
-    }
-#pragma unroll
-    for (int j = 0; j < kPerThread / 8; ++j) {
-        const int64_t e = e0 + ((int64_t)j * kAThreads + threadIdx.x) * 8;
-        if (e < e1) {
+    for (int j = 0; j < kVecs; ++j) {
+        const int64_t e = slice_vec(e0, j, lane);
+        if (FULL || e < e1) {
             float v[8];
-            if (VEC) unpack8(raw[j], v);
-            else load8<false>(z, e, a.V, v, -INFINITY);
+            vals8<VEC>(z, raw[j], e, e1, __builtin_nanf(""), v);
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
-                if (e + q < e1 && better(v[q], (int)(e + q), bv, bi)) { bv = v[q]; bi = (int)(e + q); }
+            for (int q = 0; q < 8; q += 2) zm = fmaxf(fmaxf(zm, v[q]), v[q + 1]);
         }
     }
+    return zm;
+}
+
+// (max logit, lowest index holding it) of one slice, reduced over the wave.
+template <bool VEC, bool FULL>
+__device__ __forceinline__ float2 slice_argmax(const uint16_t* z, const Raw& raw, int64_t e0, int64_t e1, int lane) {
+    const float M = wave_max(slice_max<VEC, FULL>(z, raw, e0, e1, lane));
+    // lowest index of M in the lane: scan backwards, the last hit wins
+    int bi = 0x7fffffff;
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const float ov = __shfl_xor(bv, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    for (int j = kVecs - 1; j >= 0; --j) {
+        const int64_t e = slice_vec(e0, j, lane);
+        if (FULL || e < e1) {
+            float v[8];
+            vals8<VEC>(z, raw[j], e, e1, __builtin_nanf(""), v);
+#pragma unroll
+            for (int q = 7; q >= 0; --q) bi = (v[q] == M) ? (int)(e + q) : bi;
+        }
     }
-    const int w = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) { sv[w] = bv; si[w] = bi; }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        for (int q = 1; q < kAThreads / 64; ++q)
-            if (better(sv[q], si[q], bv, bi)) { bv = sv[q]; bi = si[q]; }
-        a.stats[row * a.nchunk + c] = make_float2(bv, __int_as_float(bi));
-    }
+    return make_float2(M, __int_as_float(wave_min_i32(bi)));
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kAThreads) void greedy_partial_kernel(AcceptArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    auto row_of = [&](uint32_t row) { return a.zt + (int64_t)row * a.V; };
+    stream_items<VEC>(a, row_of, [&](uint32_t it, const Raw& raw) {
+        const uint32_t row = it / a.nslice, c = it % a.nslice;
+        const uint16_t* z = row_of(row);
+        const int64_t e0 = (int64_t)c * kSlice, e1 = min(e0 + kSlice, a.V);
+        const float2 r = (VEC && e1 - e0 == kSlice) ? slice_argmax<VEC, true>(z, raw, e0, e1, lane)
+                                                    : slice_argmax<VEC, false>(z, raw, e0, e1, lane);
+        if (lane == 0) a.stats[(int64_t)row * a.nslice + c] = r;
+    });
 }
 
 __global__ __launch_bounds__(256) void greedy_final_kernel(AcceptArgs a) {
     __shared__ int g[17];
     const int b = blockIdx.x;
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-    // wave wv merges positions wv, wv+4, ...; lanes stride over the chunks
+    // wave wv merges positions wv, wv+4, ...; lanes stride over the slices
     for (int pos = wv; pos <= a.k; pos += 4) {
-        const float2* st = a.stats + ((int64_t)b * (a.k + 1) + pos) * a.nchunk;
+        const float2* st = a.stats + ((int64_t)b * (a.k + 1) + pos) * a.nslice;
         float bv = -INFINITY;
         int bi = 0x7fffffff;
-        for (int64_t c = lane; c < a.nchunk; c += 64) {
+        for (int64_t c = lane; c < a.nslice; c += 64) {
             const float2 p = st[c];
             const int pi = __float_as_int(p.y);
             if (better(p.x, pi, bv, bi)) { bv = p.x; bi = pi; }
@@ -150,54 +222,49 @@ __global__ __launch_bounds__(256) void greedy_final_kernel(AcceptArgs a) {
 
 // ------------------------------------------------------------- stochastic
 
-template <bool VEC>
-__global__ __launch_bounds__(kAThreads) void stoch_stats_kernel(AcceptArgs a) {
-    __shared__ float red[16];
-    const int64_t c = blockIdx.x;
-    const int b = blockIdx.y / a.R;
-    const int r = blockIdx.y % a.R;
-    const uint16_t* z = (r <= a.k) ? a.zt + ((int64_t)b * (a.k + 1) + r) * a.V
-                                   : a.zd + ((int64_t)b * a.k + (r - a.k - 1)) * a.V;
-    if (c == 0 && r == 0 && threadIdx.x == 0) a.ctr[b] = 0u;   // ticket for stoch_sample_kernel
-    const int64_t e0 = c * a.chunk;
-    const int64_t e1 = min(e0 + a.chunk, a.V);
-    // Every thread streams its 8-element vectors and keeps an online
-    // (max m, sum 2^(t - m)) pair; the loads of all vectors are issued first.
-    uint4 raw[kPerThread / 8];
+// (m, sum 2^(t - m)) of t = z * c2 over one slice, reduced over the wave:
+// the wave maximum first (c2 > 0, so max t = fl(max z * c2)), then one
+// exponential per element with the wave's m, so no partial sum is rescaled.
+template <bool VEC, bool FULL>
+__device__ __forceinline__ float2 slice_stats(const uint16_t* z, const Raw& raw, int64_t e0, int64_t e1, int lane,
+                                              float c2) {
+    const float M = wave_max(slice_max<VEC, FULL>(z, raw, e0, e1, lane)) * c2;
+    float s = 0.0f;
+    if (M != -INFINITY) {
 #pragma unroll
-    for (int j = 0; j < kPerThread / 8; ++j) {
-        const int64_t e = e0 + ((int64_t)j * kAThreads + threadIdx.x) * 8;
-        if (VEC && e < e1) raw[j] = *reinterpret_cast<const uint4*>(z + e);
-    }
-    float m = -INFINITY, sum = 0.0f;
+        for (int j = 0; j < kVecs; ++j) {
+            const int64_t e = slice_vec(e0, j, lane);
+            if (FULL || e < e1) {
+                float v[8];
+                vals8<VEC>(z, raw[j], e, e1, -INFINITY, v);
 #pragma unroll
-    for (int j = 0; j < kPerThread / 8; ++j) {
-        const int64_t e = e0 + ((int64_t)j * kAThreads + threadIdx.x) * 8;
-        if (e < e1) {
-            float v[8];
-            if (VEC) unpack8(raw[j], v);
-            else load8<false>(z, e, a.V, v, 0.0f);
-            float vm = -INFINITY;
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                v[q] = (e + q < e1) ? v[q] * a.c2 : -INFINITY;
-                vm = fmaxf(vm, v[q]);
+                for (int q = 0; q < 8; ++q) s += __builtin_amdgcn_exp2f(fmaf(v[q], c2, -M));
             }
-            if (vm > m) {
-                sum = (m == -INFINITY) ? 0.0f : sum * exp2f(m - vm);
-                m = vm;
-            }
-#pragma unroll
-            for (int q = 0; q < 8; ++q) sum += exp2f(v[q] - m);
         }
     }
-    const float M = block_max(m, red);
-    float s = (m == -INFINITY) ? 0.0f : sum * exp2f(m - M);
-    s = block_sum(s, red);
-    if (threadIdx.x == 0) a.stats[((int64_t)b * a.R + r) * a.nchunk + c] = make_float2(M, s);
+    return make_float2(M, wave_sum(s));
 }
 
-// Residual (or bonus) probability of element e given the sampled position.
+template <bool VEC>
+__global__ __launch_bounds__(kAThreads) void stoch_stats_kernel(AcceptArgs a) {
+    const int lane = threadIdx.x & (kWave - 1);
+    auto row_of = [&](uint32_t row) -> const uint16_t* {
+        const int64_t b = row / a.R;
+        const int r = (int)(row % a.R);
+        return (r <= a.k) ? a.zt + (b * (a.k + 1) + r) * a.V : a.zd + (b * a.k + (r - a.k - 1)) * a.V;
+    };
+    stream_items<VEC>(a, row_of, [&](uint32_t it, const Raw& raw) {
+        const uint32_t row = it / a.nslice, c = it % a.nslice;
+        const uint16_t* z = row_of(row);
+        const int64_t e0 = (int64_t)c * kSlice, e1 = min(e0 + kSlice, a.V);
+        if (c == 0 && (row % a.R) == 0 && lane == 0) a.ctr[row / a.R] = 0u;   // ticket of the sample kernel
+        const float2 r = (VEC && e1 - e0 == kSlice) ? slice_stats<VEC, true>(z, raw, e0, e1, lane, a.c2)
+                                                    : slice_stats<VEC, false>(z, raw, e0, e1, lane, a.c2);
+        if (lane == 0) a.stats[(int64_t)row * a.nslice + c] = r;
+    });
+}
+
+// Residual (or bonus) distribution at the sampled position j.
 struct Dist {
     const uint16_t* zt_row;   // target row j
     const uint16_t* zd_row;   // draft row j, or null (one-hot drafts / bonus)
@@ -206,26 +273,124 @@ struct Dist {
     int64_t skip;             // element forced to zero (one-hot draft), -1 if none
 };
 
-template <bool VEC>
-__device__ __forceinline__ void dist8(const Dist& d, float c2, int64_t e, int64_t e1, int64_t V, float r[8]) {
+// Probabilities of the 8 elements at e (< e1) from loaded vectors: with a
+// draft row (HAS_D) the residual max(0, p - q), else p with element `skip`
+// (the one-hot draft token, or -1) set to zero.
+template <bool VEC, bool HAS_D>
+__device__ __forceinline__ void dist8(const Dist& d, float c2, const uint4& rt, const uint4& rd, int64_t e,
+                                      int64_t e1, float r[8]) {
     float zt[8];
-    load8<VEC>(d.zt_row, e, V, zt, 0.0f);
-    if (d.zd_row) {
+    vals8<VEC>(d.zt_row, rt, e, e1, 0.0f, zt);
+    if constexpr (HAS_D) {
         float zd[8];
-        load8<VEC>(d.zd_row, e, V, zd, 0.0f);
+        vals8<VEC>(d.zd_row, rd, e, e1, 0.0f, zd);
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            const float p = exp2f(zt[q] * c2 - d.mt) * d.inv_zt;
-            const float qq = exp2f(zd[q] * c2 - d.md) * d.inv_zd;
-            r[q] = (e + q < e1) ? fmaxf(p - qq, 0.0f) : 0.0f;
+            const float p = __builtin_amdgcn_exp2f(fmaf(zt[q], c2, -d.mt)) * d.inv_zt;
+            const float qq = __builtin_amdgcn_exp2f(fmaf(zd[q], c2, -d.md)) * d.inv_zd;
+            r[q] = in8<VEC>(e, q, e1) ? fmaxf(p - qq, 0.0f) : 0.0f;
         }
     } else {
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            const float p = exp2f(zt[q] * c2 - d.mt) * d.inv_zt;
-            r[q] = (e + q < e1 && e + q != d.skip) ? p : 0.0f;
+            const float p = __builtin_amdgcn_exp2f(fmaf(zt[q], c2, -d.mt)) * d.inv_zt;
+            r[q] = (in8<VEC>(e, q, e1) && e + q != d.skip) ? p : 0.0f;
         }
     }
+}
+
+// The same probability for one element e < V (bit-identical to dist8).
+template <bool HAS_D>
+__device__ __forceinline__ float dist1(const Dist& d, float c2, int64_t e) {
+    const float p = __builtin_amdgcn_exp2f(fmaf(bf16_to_f32(d.zt_row[e]), c2, -d.mt)) * d.inv_zt;
+    if constexpr (HAS_D) {
+        const float qq = __builtin_amdgcn_exp2f(fmaf(bf16_to_f32(d.zd_row[e]), c2, -d.md)) * d.inv_zd;
+        return fmaxf(p - qq, 0.0f);
+    } else {
+        return e != d.skip ? p : 0.0f;
+    }
+}
+
+// Mass of the range [e0, e1) of at most 64 elements (e0 < e1), in double.
+// The 8 vectors of the range are loaded before any is used.
+template <bool VEC, bool HAS_D>
+__device__ __forceinline__ double range_mass(const Dist& d, float c2, int64_t e0, int64_t e1) {
+    Raw rt, rd;
+    if (VEC) {
+#pragma unroll
+        for (int j = 0; j < kVecs; ++j) {
+            const int64_t e = min(e0 + j * 8, e1 - 8);
+            rt[j] = *reinterpret_cast<const uint4*>(d.zt_row + e);
+            if (HAS_D) rd[j] = *reinterpret_cast<const uint4*>(d.zd_row + e);
+        }
+    }
+    double m = 0.0;
+#pragma unroll
+    for (int j = 0; j < kVecs; ++j) {
+        const int64_t e = e0 + j * 8;
+        if (e < e1) {
+            float r[8];
+            dist8<VEC, HAS_D>(d, c2, rt[j], rd[j], e, e1, r);
+            m += (((double)r[0] + (double)r[1]) + ((double)r[2] + (double)r[3])) +
+                 (((double)r[4] + (double)r[5]) + ((double)r[6] + (double)r[7]));
+        }
+    }
+    return m;
+}
+
+// Block-wide scan of one double per thread, in thread order: the thread's
+// interval [lo, hi) of the running sum and the block total.  Intervals of
+// consecutive threads tile exactly (hi of thread t is bit-identical to lo of
+// thread t + 1), so a value in [0, total) has exactly one owner, and the
+// owner's own value is positive.  `sh` holds kWavesPerBlock doubles.
+__device__ __forceinline__ void block_scan_d(double v, double* sh, double& lo, double& hi, double& total) {
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x >> 6;
+    double incl = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const double y = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += y;
+    }
+    double excl = __shfl_up(incl, 1, kWave);
+    if (lane == 0) excl = 0.0;
+    __syncthreads();                       // sh may still be read by a previous scan
+    if (lane == kWave - 1) sh[wv] = incl;
+    __syncthreads();
+    double before = 0.0;
+    for (int q = 0; q < wv; ++q) before += sh[q];
+    double tot = before;
+    for (int q = wv; q < kWavesPerBlock; ++q) tot += sh[q];
+    lo = before + excl;
+    hi = before + incl;
+    total = tot;
+}
+
+// Owner of `target` among the block's intervals (base + [lo, hi)): writes the
+// owner's index (always in [0, blockDim.x)) and base + lo to shared memory.
+// If rounding left no owner (target at or past the end), the last thread with
+// positive mass owns it; with no positive mass at all (non-finite logits),
+// thread 0 does.
+__device__ __forceinline__ void find_owner(double v, double lo, double hi, double base, double target, int* s_own,
+                                           double* s_base, int* s_lastpos) {
+    if (threadIdx.x == 0) { *s_own = -1; *s_lastpos = -1; }
+    __syncthreads();
+    const double blo = base + lo, bhi = base + hi;
+    if (blo <= target && target < bhi) { *s_own = threadIdx.x; *s_base = blo; }
+    if (v > 0.0) atomicMax(s_lastpos, (int)threadIdx.x);
+    __syncthreads();
+    const int lastpos = *s_lastpos;
+    if (*s_own < 0 && (int)threadIdx.x == (lastpos >= 0 ? lastpos : 0)) { *s_own = threadIdx.x; *s_base = blo; }
+    __syncthreads();
+}
+
+__device__ __forceinline__ void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ void store_coherent(double* p, double v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ double load_coherent(const double* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Online merge of (max, sum 2^(t - max)) pairs.
@@ -239,54 +404,77 @@ __device__ __forceinline__ void merge_ms(float& m, float& z, float om, float oz)
     }
 }
 
+// Sampling from the residual (or bonus) distribution of position j by inverse
+// CDF in vocabulary order, in three levels: every block stores the masses of
+// its chunk's 256 ranges of 64 elements (thread t owns range t) and the chunk
+// total; the last block of the sequence finds the chunk holding u*R, then the
+// range within it, then the element within the range (one lane each).
 template <bool VEC>
 __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     __shared__ float sM[33], sZ[33];
     __shared__ int s_acc[16];
-    __shared__ int s_j, s_last, s_fallback, s_cstar;
-    __shared__ float red[16];
-    __shared__ double dsum[kAThreads / 64];
-    __shared__ double s_base, s_target;
-    __shared__ float s_mass[kMaxChunks];
-    __shared__ int s_found, s_lastnz;
+    __shared__ int s_j, s_last;
+    __shared__ double sh[kWavesPerBlock];
+    __shared__ int s_own, s_lastpos;
+    __shared__ double s_base;
     const int64_t c = blockIdx.x;
     const int b = blockIdx.y;
     const int t = threadIdx.x;
     const int lane = t & 63, wv = t >> 6;
     const int k = a.k;
 
-    // 1. merge the chunk statistics of every row of sequence b: wave wv takes
-    //    rows wv, wv+4, ...; lanes stride over chunks; fixed shuffle tree.
-    for (int r = wv; r < a.R; r += kAThreads / 64) {
-        const float2* st = a.stats + ((int64_t)b * a.R + r) * a.nchunk;
-        float m = -INFINITY, z = 0.0f;
-        for (int64_t q = lane; q < a.nchunk; q += 64) {
-            const float2 v = st[q];
-            merge_ms(m, z, v.x, v.y);
+    // The operands of the accept tests are loaded first (draft id, then the
+    // two logits at it), so their round trips overlap the statistics merge.
+    int32_t xi = -1;
+    float zx_t = 0.0f, zx_d = 0.0f, ui = 0.0f;
+    if (t < k) {
+        xi = a.x[(int64_t)b * k + t];
+        ui = a.u[(int64_t)b * (k + 1) + t];
+        if (xi >= 0 && xi < a.V) {
+            zx_t = bf16_to_f32(a.zt[((int64_t)b * (k + 1) + t) * a.V + xi]);
+            if (a.zd) zx_d = bf16_to_f32(a.zd[((int64_t)b * k + t) * a.V + xi]);
         }
-        const float M = wave_max(m);
-        const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));
-        if (lane == 0) { sM[r] = M; sZ[r] = Z; }
+    }
+
+    // 1. merge the slice statistics of every row of sequence b: wave wv takes
+    //    rows wv, wv+4, ...; lanes stride over slices (the first slice of
+    //    every row is loaded up front); fixed reduction order.
+    constexpr int kRowsPerWave = (33 + kWavesPerBlock - 1) / kWavesPerBlock;   // R <= 2*16+1
+    float2 first[kRowsPerWave];
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave; ++i) {
+        const int r = wv + i * kWavesPerBlock;
+        first[i] = (r < (int)a.R && lane < (int)a.nslice) ? a.stats[((int64_t)b * a.R + r) * a.nslice + lane]
+                                                          : make_float2(-INFINITY, 0.0f);
+    }
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave; ++i) {
+        const int r = wv + i * kWavesPerBlock;
+        if (r < (int)a.R) {
+            const float2* st = a.stats + ((int64_t)b * a.R + r) * a.nslice;
+            float m = -INFINITY, z = 0.0f;
+            merge_ms(m, z, first[i].x, first[i].y);
+            for (int64_t q = lane + kWave; q < a.nslice; q += kWave) {
+                const float2 v = st[q];
+                merge_ms(m, z, v.x, v.y);
+            }
+            const float M = wave_max(m);
+            const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));
+            if (lane == 0) { sM[r] = M; sZ[r] = Z; }
+        }
     }
     __syncthreads();
 
     // 2. accept tests of the k drafts, evaluated in parallel (identical in
     //    every block of sequence b); the first rejection j is then a scan.
+    //    t - M is formed exactly in double (bf16 * fp32 fits in 53 bits).
     if (t < k) {
-        const int32_t xi = a.x[(int64_t)b * k + t];
         double p = 0.0, q = 0.0;
         if (xi >= 0 && xi < a.V) {
-            const float zt = bf16_to_f32(a.zt[((int64_t)b * (k + 1) + t) * a.V + xi]);
-            p = exp2((double)(zt * a.c2) - (double)sM[t]) / (double)sZ[t];
-            if (a.zd) {
-                const float zd = bf16_to_f32(a.zd[((int64_t)b * k + t) * a.V + xi]);
-                q = exp2((double)(zd * a.c2) - (double)sM[k + 1 + t]) / (double)sZ[k + 1 + t];
-            } else {
-                q = 1.0;
-            }
+            p = exp2((double)zx_t * (double)a.c2 - (double)sM[t]) / (double)sZ[t];
+            q = a.zd ? exp2((double)zx_d * (double)a.c2 - (double)sM[k + 1 + t]) / (double)sZ[k + 1 + t] : 1.0;
         }
-        const double ui = (double)a.u[(int64_t)b * (k + 1) + t];
-        s_acc[t] = (ui * q < p) ? 1 : 0;
+        s_acc[t] = ((double)ui * q < p) ? 1 : 0;
     }
     __syncthreads();
     if (t == 0) {
@@ -316,161 +504,100 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
         }
     }
 
-    // 3. residual mass of this chunk
-    const int64_t e0 = c * a.chunk;
-    const int64_t e1 = min(e0 + a.chunk, a.V);
-    float part = 0.0f;
-#pragma unroll
-    for (int jj = 0; jj < kPerThread / 8; ++jj) {
-        const int64_t e = e0 + ((int64_t)jj * kAThreads + t) * 8;
-        if (e < e1) {
-            float r[8];
-            dist8<VEC>(d, a.c2, e, e1, a.V, r);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) part += r[q];
-        }
-    }
-    part = block_sum(part, red);
-    if (t == 0) {
-        a.mass[(int64_t)b * a.nchunk + c] = part;
-        __threadfence();
-        const unsigned int ticket = atomicAdd(a.ctr + b, 1u);
-        s_last = (ticket == (unsigned int)(a.nchunk - 1));
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
+    double* cm = a.chunkm + (int64_t)b * a.nchunk;              // chunk masses
+    double* fm = a.finem + (int64_t)b * a.nchunk * kAThreads;   // range masses
+    auto range_of = [&](int64_t ch, int th, int64_t& e0, int64_t& e1) {
+        e0 = ch * kChunk + (int64_t)th * kPerThread;
+        e1 = min(e0 + kPerThread, a.V);
+    };
+    auto mass_of = [&](int64_t ch) {
+        int64_t e0, e1;
+        range_of(ch, t, e0, e1);
+        if (e0 >= a.V) return 0.0;
+        return d.zd_row ? range_mass<VEC, true>(d, a.c2, e0, e1) : range_mass<VEC, false>(d, a.c2, e0, e1);
+    };
 
-    // 4. last block of sequence b: gather the chunk masses (if the residual
-    //    vanished through rounding, the chunk masses of p_j instead), find the
-    //    chunk holding u*R, then scan that chunk in vocabulary order.
+    // 3. this block's range masses and chunk total, stored device-coherently
+    //    (relaxed agent-scope atomic stores, written through the L2) and
+    //    acknowledged before the ticket is taken; the last block reads them
+    //    with device-coherent loads.  No agent-scope fence is needed (on this
+    //    chip such a fence writes back and invalidates the XCD's whole L2).
     {
-        const float* ms = a.mass + (int64_t)b * a.nchunk;
-        float mine = 0.0f;
-        for (int64_t q = t; q < a.nchunk; q += kAThreads) {
-            const float v = __hip_atomic_load(ms + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            s_mass[q] = v;
-            mine += v;
+        const double m = mass_of(c);
+        store_coherent(fm + c * kAThreads + t, m);
+        double lo, hi, tot;
+        block_scan_d(m, sh, lo, hi, tot);
+        if (t == 0) store_coherent(cm + c, tot);
+        wait_stores();
+        __syncthreads();
+        if (t == 0) {
+            const unsigned int ticket = __hip_atomic_fetch_add(a.ctr + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_last = (ticket == (unsigned int)(a.nchunk - 1));
         }
-        const float R = block_sum(mine, red);
-        if (t == 0) s_fallback = !(R > 0.0f);
+        __syncthreads();
+        if (!s_last) return;
     }
-    __syncthreads();
-    if (s_fallback) {
-        const float2* st = a.stats + ((int64_t)b * a.R + j) * a.nchunk;
-        for (int64_t q = t; q < a.nchunk; q += kAThreads) {
-            const float2 v = st[q];
-            s_mass[q] = v.x == -INFINITY ? 0.0f : v.y * exp2f(v.x - d.mt) * d.inv_zt;
-        }
+
+    // 4. last block of sequence b.  Level 1: the chunk holding u*R.
+    double v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
+    double lo1, hi1, R;
+    block_scan_d(v1, sh, lo1, hi1, R);
+    if (!(R > 0.0)) {
+        // The residual vanished (p_j == q_j wherever it is positive): sample
+        // p_j itself.  This block recomputes every range and chunk mass.
         d.zd_row = nullptr;
         d.skip = -1;
-        __syncthreads();
-    }
-    if (wv == 0) {
-        // wave 0: prefix over chunk masses in double (lane l owns a contiguous run)
-        const int64_t per = (a.nchunk + 63) / 64;
-        const int64_t q0 = lane * per, q1 = min(q0 + per, a.nchunk);
-        double loc = 0.0;
-        int64_t lastpos = -1;
-        for (int64_t q = q0; q < q1; ++q) {
-            loc += (double)s_mass[q];
-            if (s_mass[q] > 0.0f) lastpos = q;
+        for (int64_t ch = 0; ch < a.nchunk; ++ch) {
+            const double m = mass_of(ch);
+            store_coherent(fm + ch * kAThreads + t, m);
+            double lo, hi, tot;
+            block_scan_d(m, sh, lo, hi, tot);
+            if (t == 0) store_coherent(cm + ch, tot);
         }
-        double incl = loc;
+        wait_stores();
+        __syncthreads();
+        v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
+        block_scan_d(v1, sh, lo1, hi1, R);
+    }
+    const double target = (double)a.u[(int64_t)b * (k + 1) + k] * R;
+    find_owner(v1, lo1, hi1, 0.0, target, &s_own, &s_base, &s_lastpos);
+    const int64_t cs = s_own;
+    const double base2 = s_base;
+
+    // Level 2: the range of 64 elements within chunk cs.
+    const double v2 = load_coherent(fm + cs * kAThreads + t);
+    double lo2, hi2, tot2;
+    block_scan_d(v2, sh, lo2, hi2, tot2);
+    find_owner(v2, lo2, hi2, base2, target, &s_own, &s_base, &s_lastpos);
+
+    // Level 3: the element within the range (wave 0, one element per lane).
+    if (wv == 0) {
+        int64_t e0, e1;
+        range_of(cs, s_own, e0, e1);
+        const double base3 = s_base;
+        const int64_t e = e0 + lane;
+        const float r = e < e1 ? (d.zd_row ? dist1<true>(d, a.c2, e) : dist1<false>(d, a.c2, e)) : 0.0f;
+        double incl = (double)r;
 #pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const double y = __shfl_up(incl, o, 64);
+        for (int o = 1; o < kWave; o <<= 1) {
+            const double y = __shfl_up(incl, o, kWave);
             if (lane >= o) incl += y;
         }
-        const double R = __shfl(incl, 63, 64);
-        const double target = (double)a.u[(int64_t)b * (k + 1) + k] * R;
-        double cum = incl - loc;
-        int64_t cstar = -1;
-        double base = 0.0;
-        for (int64_t q = q0; q < q1; ++q) {
-            const double mq = (double)s_mass[q];
-            if (cstar < 0 && cum + mq > target) { cstar = q; base = cum; }
-            cum += mq;
-        }
-        // the first lane (in vocabulary order) that found the crossing wins
-        unsigned long long hit = __ballot(cstar >= 0);
-        int64_t lastall = lastpos;
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) {
-            const int64_t y = __shfl_xor(lastall, o, 64);
-            lastall = y > lastall ? y : lastall;
-        }
-        if (hit) {
-            const int src = __ffsll((long long)hit) - 1;
-            const int64_t cs = __shfl(cstar, src, 64);
-            const double bs = __shfl(base, src, 64);
-            if (lane == 0) { s_cstar = (int)cs; s_base = bs; }
-        } else if (lane == 0) {
-            s_cstar = (int)(lastall >= 0 ? lastall : 0);   // u*R beyond the total (rounding)
-            s_base = R;
-        }
-        if (lane == 0) s_target = target;
-    }
-    if (t == 0) { s_found = 0x7fffffff; s_lastnz = -1; }
-    __syncthreads();
-    const int64_t cs = s_cstar;
-    const double tgt = s_target - s_base;
-    const int64_t f0 = cs * a.chunk;
-    const int64_t f1 = min(f0 + a.chunk, a.V);
-    // contiguous ownership: thread t scans elements [f0 + 128t, f0 + 128t + 128).
-    // Pass 1: per-thread sums; exclusive scan across the block; pass 2: the
-    // thread whose range holds the crossing walks its elements again.
-    double mine = 0.0;
-    int lastnz = -1;
-#pragma unroll 4
-    for (int jj = 0; jj < kPerThread / 8; ++jj) {
-        const int64_t e = f0 + (int64_t)t * kPerThread + jj * 8;
-        if (e < f1) {
-            float r[8];
-            dist8<VEC>(d, a.c2, e, f1, a.V, r);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                mine += (double)r[q];
-                if (r[q] > 0.0f) lastnz = (int)(e + q);
+        double excl = __shfl_up(incl, 1, kWave);
+        if (lane == 0) excl = 0.0;
+        const unsigned long long own = __ballot(base3 + excl <= target && target < base3 + incl);
+        const unsigned long long pos = __ballot(r > 0.0f);
+        int pick;
+        if (own) pick = __ffsll((long long)own) - 1;
+        else if (pos) pick = 63 - __builtin_clzll(pos);          // rounding: last positive element
+        else pick = 0;
+        if (lane <= k) {
+            int32_t* out = a.out + (int64_t)b * (k + 1);
+            out[lane] = lane < j ? a.x[(int64_t)b * k + lane] : (lane == j ? (int)min(e0 + pick, a.V - 1) : -1);
+            if (lane == 0) {
+                a.num[b] = j;
+                a.ctr[b] = 0u;
             }
-        }
-    }
-    double incl = mine;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const double y = __shfl_up(incl, o, 64);
-        if (lane >= o) incl += y;
-    }
-    if (lane == 63) dsum[wv] = incl;
-    __syncthreads();
-    double before = 0.0;
-    for (int q = 0; q < wv; ++q) before += dsum[q];
-    double cum = before + incl - mine;
-    int found = -1;
-    if (cum <= tgt && cum + mine > tgt) {
-        for (int jj = 0; jj < kPerThread / 8 && found < 0; ++jj) {
-            const int64_t e = f0 + (int64_t)t * kPerThread + jj * 8;
-            if (e < f1) {
-                float r[8];
-                dist8<VEC>(d, a.c2, e, f1, a.V, r);
-                for (int q = 0; q < 8; ++q) {
-                    cum += (double)r[q];
-                    if (found < 0 && e + q < f1 && cum > tgt) found = (int)(e + q);
-                }
-            }
-        }
-    }
-    if (found >= 0) atomicMin(&s_found, found);
-    if (lastnz >= 0) atomicMax(&s_lastnz, lastnz);
-    __syncthreads();
-    if (t <= k) {
-        int tok = s_found;
-        if (tok == 0x7fffffff) tok = s_lastnz >= 0 ? s_lastnz : (int)f0;
-        int32_t* out = a.out + (int64_t)b * (k + 1);
-        out[t] = t < j ? a.x[(int64_t)b * k + t] : (t == j ? tok : -1);
-        if (t == 0) {
-            a.num[b] = j;
-            a.ctr[b] = 0u;
         }
     }
 }
@@ -482,13 +609,16 @@ inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {
     AcceptPlan p{};
     p.chunk = kChunk;
-    if (V < p.chunk) p.chunk = (V + 7) / 8 * 8;
-    p.nchunk = (V + p.chunk - 1) / p.chunk;
+    p.nchunk = (V + kChunk - 1) / kChunk;
+    p.schunk = kSlice;
+    p.nschunk = (V + kSlice - 1) / kSlice;
     const int64_t R = 2 * k + 1;
     p.stats_off = 0;
-    p.mass_off = align256((size_t)B * R * p.nchunk * sizeof(float2));
-    p.ctr_off = p.mass_off + align256((size_t)B * p.nchunk * sizeof(float));
+    p.mass_off = align256((size_t)B * R * p.nschunk * sizeof(float2));
+    p.fine_off = p.mass_off + align256((size_t)B * p.nchunk * sizeof(double));
+    p.ctr_off = p.fine_off + align256((size_t)B * p.nchunk * kAThreads * sizeof(double));
     p.bytes = p.ctr_off + align256((size_t)B * sizeof(unsigned int));
+    if (B == 0) p.bytes = 0;
     return p;
 }
 
@@ -499,26 +629,29 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
     char* ws = reinterpret_cast<char*>(workspace);
     a.zt = zt; a.zd = zd; a.x = x; a.u = u; a.out = out_tokens; a.num = num_accepted;
     a.stats = reinterpret_cast<float2*>(ws + p.stats_off);
-    a.mass = reinterpret_cast<float*>(ws + p.mass_off);
+    a.chunkm = reinterpret_cast<double*>(ws + p.mass_off);
+    a.finem = reinterpret_cast<double*>(ws + p.fine_off);
     a.ctr = reinterpret_cast<unsigned int*>(ws + p.ctr_off);
-    a.V = V; a.chunk = p.chunk; a.nchunk = p.nchunk; a.B = (int)B; a.k = (int)k;
+    a.V = V; a.nchunk = p.nchunk; a.nslice = (uint32_t)p.nschunk; a.B = (int)B; a.k = (int)k;
     const bool vec = (V % 8 == 0) && ((uintptr_t)zt % 16 == 0) && (zd == nullptr || (uintptr_t)zd % 16 == 0);
     if (temperature == 0.0f) {
-        a.R = (int)(k + 1);
+        a.R = (uint32_t)(k + 1);
         a.c2 = 0.0f;
-        dim3 g1((unsigned)p.nchunk, (unsigned)(B * (k + 1)));
-        if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, g1, dim3(kAThreads), 0, stream, a);
-        else hipLaunchKernelGGL(greedy_partial_kernel<false>, g1, dim3(kAThreads), 0, stream, a);
+        a.items = (uint32_t)(B * a.R * p.nschunk);
+        const unsigned g1 = (unsigned)((stream_waves(a.items) + kWavesPerBlock - 1) / kWavesPerBlock);
+        if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
+        else hipLaunchKernelGGL(greedy_partial_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(greedy_final_kernel, dim3((unsigned)B), dim3(256), 0, stream, a);
         return hipGetLastError();
     }
-    a.R = (int)((k + 1) + (zd ? k : 0));
+    a.R = (uint32_t)((k + 1) + (zd ? k : 0));
     a.c2 = (float)(1.4426950408889634 / (double)temperature);
-    dim3 g1((unsigned)p.nchunk, (unsigned)(B * a.R));
-    if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, g1, dim3(kAThreads), 0, stream, a);
-    else hipLaunchKernelGGL(stoch_stats_kernel<false>, g1, dim3(kAThreads), 0, stream, a);
+    a.items = (uint32_t)(B * a.R * p.nschunk);
+    const unsigned g1 = (unsigned)((stream_waves(a.items) + kWavesPerBlock - 1) / kWavesPerBlock);
+    if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
+    else hipLaunchKernelGGL(stoch_stats_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g2((unsigned)p.nchunk, (unsigned)B);

@@ -47,16 +47,41 @@ __device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
     return (uint32_t)r;
 }
 
+// Wave-wide reductions on DPP lane permutations (VALU operand modifiers, no
+// LDS round trip): xor 1 and xor 2 inside quads, then the half-row and row
+// mirrors leave every lane of a 16-lane row with the row's total; the four
+// row totals are read as scalars and combined in a fixed order.  The result
+// is wave-uniform and deterministic.  All 64 lanes must be active.
+template <int CTRL>
+__device__ __forceinline__ int dpp_mov(int v) {
+    return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, false);
+}
+
+template <class Op>
+__device__ __forceinline__ int wave_reduce_i(int v, Op op) {
+    v = op(v, dpp_mov<0xB1>(v));    // quad_perm [1,0,3,2]
+    v = op(v, dpp_mov<0x4E>(v));    // quad_perm [2,3,0,1]
+    v = op(v, dpp_mov<0x141>(v));   // row_half_mirror
+    v = op(v, dpp_mov<0x140>(v));   // row_mirror
+    const int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return op(op(r0, r1), op(r2, r3));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-    return v;
+    return __builtin_bit_cast(float, wave_reduce_i(__builtin_bit_cast(int, v), [](int a, int b) {
+        return __builtin_bit_cast(int, fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)));
+    }));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
-    return v;
+    return __builtin_bit_cast(float, wave_reduce_i(__builtin_bit_cast(int, v), [](int a, int b) {
+        return __builtin_bit_cast(int, __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b));
+    }));
+}
+
+__device__ __forceinline__ int wave_min_i32(int v) {
+    return wave_reduce_i(v, [](int a, int b) { return a < b ? a : b; });
 }
 
 __device__ __forceinline__ double wave_sum_d(double v) {

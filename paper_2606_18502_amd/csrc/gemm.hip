@@ -451,10 +451,16 @@ hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
 
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
     GemmPlan p{};
+    // Tile shapes by measurement on MI355X (M = B*(k+1) verify rows):
+    //   M <= 64: 64x64;  M <= 80: 80x128;
+    //   M <= 320: 160x224 when N fills >= 64 such columns exactly (gate|up),
+    //             160x128 with a K split for long-K layers (down), else
+    //             160x64 (QKV, O: more tiles, no split);
+    //   larger M: 160x224.
     if (M <= 64) p.kind = 0;
     else if (M <= 80) p.kind = 1;
-    else if (M <= 320) p.kind = (N % 224 == 0 && N >= 224 * 64) ? 2 : (N % 192 == 0 ? 4 : 5);
-    else p.kind = 3;
+    else if (M <= 320) p.kind = (N % 224 == 0 && N >= 224 * 64) ? 2 : (K >= 2 * N ? 5 : 7);
+    else p.kind = 2;
     const int ksteps = (int)(K / kBK);
     int splits = 0;
 #ifdef SPECFP8_TUNING
@@ -469,11 +475,11 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
     p.n_tiles = (int)((N + bn - 1) / bn);
     const int tiles = p.m_tiles * p.n_tiles;
     if (splits <= 0) {
-        // Split K only when fewer than half of the 256 compute units would
-        // get a tile, and never beyond one wave of workgroups: every split
+        // Split K only when at most half of the 256 compute units would get
+        // a tile, and keep the split grid under ~200 workgroups: every split
         // adds an M x N fp32 partial that is written and read back.
         splits = 1;
-        if (2 * tiles <= 256) splits = 256 / tiles;
+        if (2 * tiles <= 256) splits = 200 / tiles;
         const int max_split = ksteps / 4 > 0 ? ksteps / 4 : 1;   // >= 4 K-steps per split
         if (splits > max_split) splits = max_split;
         if (splits > 16) splits = 16;

@@ -29,9 +29,11 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
 
 // ---- accept.hip
 struct AcceptPlan {
-    int64_t chunk;         // vocabulary elements per workgroup
-    int64_t nchunk;        // chunks per row
-    size_t stats_off, mass_off, ctr_off, bytes;
+    int64_t chunk;         // vocabulary elements per sampling workgroup
+    int64_t nchunk;        // sampling chunks per row
+    int64_t schunk;        // vocabulary elements per statistics item (one wave)
+    int64_t nschunk;       // statistics items per row
+    size_t stats_off, mass_off, fine_off, ctr_off, bytes;
 };
 AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V);
 hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t* zd, const int32_t* x,

@@ -8,7 +8,7 @@
 // derives the scale, and encodes the registers it already holds.  HBM traffic
 // is therefore the algorithmic 2 bytes in + 1 byte out per element (4 + 1 for
 // the SiLU-gated input) plus 4 bytes of scale per row.  Rows wider than
-// 16384 elements take a second pass that re-reads the row.
+// 65536 elements take a second pass that re-reads the row.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -16,11 +16,17 @@ namespace specfp8 {
 
 namespace {
 
-constexpr int kQThreads = 256;
+constexpr int kQThreads = 256;       // threads of the element-wise kernel
+constexpr int kQMaxThreads = 1024;   // threads per row of the row kernel, at most
 
-// h = bf16(silu(g) * u), silu(g) = g / (1 + e^-g), computed in fp32.
+// h = bf16(silu(g) * u) with silu(g) = g / (1 + e^-g) = g * rcp(1 + 2^(-g log2 e)),
+// in fp32 on the hardware exp2 and reciprocal (about 1 ulp each): the bf16
+// rounding of h only differs from an exact evaluation at near-ties.  Large
+// |g| saturate correctly: 2^(+big) = inf gives rcp = 0 (silu -> -0), and
+// 2^(-big) = 0 gives silu = g.
 __device__ __forceinline__ float silu_mul_bf16(float g, float u) {
-    const float sg = g / (1.0f + expf(-g));
+    const float e = __builtin_amdgcn_exp2f(g * -1.44269504088896341f);
+    const float sg = g * __builtin_amdgcn_rcpf(1.0f + e);
     return bf16_to_f32(f32_to_bf16_rne(sg * u));
 }
 
@@ -59,7 +65,7 @@ __device__ __forceinline__ void row_scale(float amax, float* s_out, float* inv_o
 // NCH > 0: the row lives in registers (NCH chunks of 8 per thread).
 // NCH == 0: rows too wide for registers; amax pass and encode pass each read the row.
 template <int IN_KIND, int MODE, int NCH>
-__global__ __launch_bounds__(kQThreads) void quantize_rows_kernel(
+__global__ __launch_bounds__(kQMaxThreads) void quantize_rows_kernel(
     const uint16_t* __restrict__ x, int64_t cols, int64_t ld_x, float* __restrict__ scales,
     uint8_t* __restrict__ q, int64_t ld_q) {
     __shared__ float red[16];
@@ -141,9 +147,13 @@ __global__ __launch_bounds__(kQThreads) void silu_mul_bf16_kernel(
 template <int IN_KIND, int MODE>
 hipError_t launch_quantize_t(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x,
                              float* scales, uint8_t* q, int64_t ld_q, hipStream_t stream) {
+    // One workgroup per row, wide enough that a thread holds at most 4
+    // chunks of 8 (up to 1024 threads; wider rows hold up to 8 per thread or
+    // take the two-pass path).
     const int64_t nchunks = cols / 8;
-    int threads = kQThreads;
-    if (nchunks < kQThreads) threads = (int)(((nchunks + 63) / 64) * 64);
+    int threads = 256;
+    while (threads < kQMaxThreads && nchunks > 4 * (int64_t)threads) threads *= 2;
+    if (nchunks < threads) threads = (int)(((nchunks + 63) / 64) * 64);
     const int64_t per = (nchunks + threads - 1) / threads;
     dim3 grid((unsigned)rows), block(threads);
 #define SPEC_Q_CASE(N)                                                                        \

@@ -66,7 +66,7 @@ spec_status check_accept(const void* target_logits, const void* draft_logits, co
     (void)draft_logits;
     if (!isfinite(temperature) || temperature < 0.0f) return SPEC_ERR_VALUE;
     if (B < 0 || k < 1 || V < 1) return SPEC_ERR_SHAPE;
-    if (k > 16 || V > 8388608LL) return SPEC_ERR_UNSUPPORTED;   // 1024 chunks of 8192
+    if (k > 16 || V > 4194304LL) return SPEC_ERR_UNSUPPORTED;   // <= 256 sampling chunks of 16384
     if (B * (2 * k + 1) > kMaxGridY) return SPEC_ERR_UNSUPPORTED;
     if (B == 0) return SPEC_OK;
     if (!target_logits || !draft_tokens || !out_tokens || !num_accepted) return SPEC_ERR_NULL;

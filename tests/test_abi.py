@@ -122,7 +122,8 @@ def test_accept_validation(lib):
     assert acc(lib, V=0) == SHAPE
     assert acc(lib, k=17) == UNSUP
     assert acc(lib, V=1 << 31) == UNSUP
-    assert acc(lib, V=(1 << 23) + 1) == UNSUP
+    assert acc(lib, V=(1 << 22) + 8) == UNSUP
+    assert acc(lib, V=1 << 22, ws=None) == WS        # the largest V passes the shape checks
     assert acc(lib, B=20000, k=4) == UNSUP
     assert acc(lib, zt=None) == NULL
     assert acc(lib, x=None) == NULL

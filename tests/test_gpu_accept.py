@@ -48,6 +48,7 @@ def _stochastic_case(B, k, V, seed, c, T, with_draft=True, scale=2.0):
     (33, 4, 20000, 3, 0.99),        # several vocabulary chunks, ragged last chunk
     (3, 16, 64, 4, 0.7),            # longest chain
     (4, 1, 1, 5, 0.5),              # one-token vocabulary
+    (2, 1, 1 << 22, 6, 0.9),        # largest vocabulary (1024 slices, 256 sampling chunks)
 ])
 def test_greedy_bit_exact(B, k, V, seed, c):
     p = need_gpu()
@@ -170,3 +171,94 @@ def test_deterministic():
     b = [host(t) for t in p.verify_accept(*args)]
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1], b[1])
+
+
+def _sample_position_ok(out, num, zt, zd, x, u, T, tol=1e-5):
+    """Every emitted sample lies at the oracle's inverse-CDF position of u*R up
+    to tol*R of cumulative mass (the fp32 probabilities move the boundaries by
+    about 1e-6 R), and carries positive residual mass."""
+    B, k1, V = zt.shape
+    k = k1 - 1
+    for b in range(B):
+        a = int(num[b])
+        v = int(out[b, a])
+        p = oa.softmax64(zt[b, a], T)
+        if a < k:
+            q = None if zd is None else oa.softmax64(zd[b, a], T)
+            r = p.copy() if q is None else np.maximum(p - q, 0)
+            if q is None and 0 <= x[b, a] < V:
+                r[x[b, a]] = 0
+            if not r.sum() > 0:
+                r = p
+        else:
+            r = p
+        cum = np.cumsum(r)
+        R = cum[-1]
+        t = float(u[b, k]) * R
+        assert r[v] > 0, (b, v)
+        lo = cum[v - 1] if v > 0 else 0.0
+        assert lo <= t + tol * R and cum[v] >= t - tol * R, (b, v, lo / R, cum[v] / R, t / R)
+
+
+def test_vanished_residual_samples_target():
+    """p_j == q_j and an out-of-range draft: the rejection's residual is
+    identically zero, so the token is drawn from p_j itself (several chunks)."""
+    p = need_gpu()
+    B, k, V, T = 16, 4, 40000, 0.7
+    zt, _ = wl.accept_logits(B, k, V, 12, 0.5)
+    zd = np.ascontiguousarray(zt[:, :k])
+    x = wl.draft_tokens_sampled(zd, T, seed=5)
+    x[0::2, 1] = V + 3                       # rejected at position <= 1, residual 0
+    x[1::4, 0] = -2
+    u = wl.philox_uniforms((B, k + 1), seed=6)
+    out, num = p.verify_accept(dev_bf16(zt), dev_bf16(zd), dev_i32(x), dev_f32(u), T)
+    out, num = host(out), host(num)
+    out_ref, num_ref, mg = oa.accept_stochastic(zt, zd, x, u, T, return_margins=True)
+    np.testing.assert_array_equal(num, num_ref)
+    assert np.all(num[0::2] <= 1) and np.all(num[1::4] == 0)
+    clear = mg > MARGIN
+    assert clear.mean() >= 0.5
+    np.testing.assert_array_equal(out[clear], out_ref[clear])
+    _check_valid(out, num, x, V)
+    _sample_position_ok(out, num, zt, zd, x, u, T)
+
+
+def test_extreme_uniforms():
+    """u = 0 draws the first token of positive residual mass (exactly); u just
+    below 1 draws at the top of the CDF (ragged last chunk, scalar path too)."""
+    p = need_gpu()
+    T = 0.7
+    for V in (20000, 20001):
+        B, k = 8, 3
+        zt, zd = wl.accept_logits(B, k, V, 13, 0.3)
+        x = wl.draft_tokens_sampled(zd, T, seed=7)
+        u = wl.philox_uniforms((B, k + 1), seed=8)
+        u[:, 0] = 1.0 - 2.0 ** -24            # reject position 0 whenever p < q there
+        u[0::2, k] = 0.0
+        u[1::2, k] = np.float32(1.0 - 2.0 ** -24)
+        out, num = p.verify_accept(dev_bf16(zt), dev_bf16(zd), dev_i32(x), dev_f32(u), T)
+        out, num = host(out), host(num)
+        out_ref, num_ref = oa.accept_stochastic(zt, zd, x, u, T)
+        np.testing.assert_array_equal(num, num_ref)
+        np.testing.assert_array_equal(out[0::2], out_ref[0::2])
+        _check_valid(out, num, x, V)
+        _sample_position_ok(out, num, zt, zd, x, u, T)
+
+
+def test_stochastic_largest_vocabulary():
+    """V = 2^22 (256 sampling chunks): accept decisions match, and every sample
+    sits at its inverse-CDF position within the fp32 error."""
+    p = need_gpu()
+    B, k, V, T = 2, 2, 1 << 22, 0.7
+    say("stochastic V=2^22")
+    zt, zd = wl.accept_logits(B, k, V, 14, 0.9)
+    x = wl.draft_tokens_sampled(zd, T, seed=9)
+    u = wl.philox_uniforms((B, k + 1), seed=10)
+    out, num = p.verify_accept(dev_bf16(zt), dev_bf16(zd), dev_i32(x), dev_f32(u), T)
+    out, num = host(out), host(num)
+    px, qx = oa.accept_probabilities(zt, zd, x, T)
+    for b in range(B):                       # decisions are far from their boundaries here
+        acc = [float(u[b, i]) * qx[b, i] < px[b, i] for i in range(k)]
+        assert num[b] == (acc.index(False) if False in acc else k)
+    _check_valid(out, num, x, V)
+    _sample_position_ok(out, num, zt, zd, x, u, T)
