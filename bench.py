@@ -98,54 +98,53 @@ class Step:
         self.out = torch.empty((B, k + 1), dtype=torch.int32, device=dev)
         self.num = torch.empty((B,), dtype=torch.int32, device=dev)
 
-    def run(self, weights, logits, ev=None):
+    def run(self, weights, logits):
         p = self.p
         for name in ("qkv", "o", "gate_up"):
             p.quantize(self.acts[name], out=self.q[name], scales=self.s[name])
-            if ev is not None and name == "gate_up":
-                ev["gu"][0].record()
             w, sw = weights[name]
             p.gemm(self.q[name], self.s[name], w, sw, out=self.y[name], workspace=self.gws)
-            if ev is not None and name == "gate_up":
-                ev["gu"][1].record()
         p.quantize(self.y["gate_up"], silu_mul=True, out=self.q["down"], scales=self.s["down"])
         w, sw = weights["down"]
         p.gemm(self.q["down"], self.s["down"], w, sw, out=self.y["down"], workspace=self.gws)
         zt, zd, x, u = logits
-        if ev is not None:
-            ev["acc"][0].record()
         p.verify_accept(zt, zd, x, u, self.T, workspace=self.aws, out_tokens=self.out, num_accepted=self.num)
-        if ev is not None:
-            ev["acc"][1].record()
 
 
 def time_parts(torch, step, weights, logits, reps):
-    """Per-part event timing (quantize+GEMM per linear, accept), median over reps."""
+    """Per-part event timing: each part (one GEMM, or the acceptance) is
+    launched `reps` times back to back on the current stream, every launch
+    bracketed by HIP events, so the GPU never waits for the host between
+    them; returns the mean launch duration in us per part."""
     p = step.p
     names = ["qkv", "o", "gate_up", "down", "accept"]
-    ts = {n: [] for n in names}
-    for r in range(reps):
-        w = weights[r % len(weights)]
-        lg = logits[r % len(logits)]
-        for n in names:
+    res = {}
+    for n in names:
+        evs = []
+        for r in range(reps):
+            w = weights[r % len(weights)]
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
             if n == "accept":
-                zt, zd, x, u = lg
+                zt, zd, x, u = logits[r % len(logits)]
                 p.verify_accept(zt, zd, x, u, step.T, workspace=step.aws, out_tokens=step.out,
                                 num_accepted=step.num)
-            elif n == "down":
-                p.gemm(step.q["down"], step.s["down"], *w["down"], out=step.y["down"], workspace=step.gws)
             else:
                 p.gemm(step.q[n], step.s[n], *w[n], out=step.y[n], workspace=step.gws)
             e1.record()
-            ts[n].append((e0, e1))
-    torch.cuda.synchronize()
-    return {n: float(np.median([a.elapsed_time(b) for a, b in v])) * 1e3 for n, v in ts.items()}
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        res[n] = float(np.mean([a.elapsed_time(b) for a, b in evs[2:]])) * 1e3
+    return res
 
 
-def cpu_baseline(wl):
-    """The oracle on a bounded sample of the same workload, on the host cores."""
+def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=12):
+    """The oracle on the host cores, on a bounded sample of the benched step:
+    the 4 linears at M=320 restricted to every `nfrac`-th output channel
+    (full K; per-token quantize, the SiLU-gated re-quantize of a full-width
+    gate|up output, exact fp64 GEMMs on the decoded operands) and stochastic
+    acceptance of all 64 sequences at full vocabulary, repeated until at least
+    `min_seconds` have passed.  `value` is GEMM FLOPs per second."""
     from oracle import accept as oa, gemm as og, quantize as oq
     try:
         from threadpoolctl import threadpool_info
@@ -153,42 +152,40 @@ def cpu_baseline(wl):
     except Exception:
         threads = os.cpu_count() or 1
     cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
-    rows, nfrac, bseq = 16, 8, 8
     M = cfg3["M"]
-    # untimed: sampled activations, weights for every nfrac-th output channel, oracle-quantized
-    xs = {}
+    xs, wq = {}, {}
     for i, (name, N, K) in enumerate(cfg3["linears"]):
-        if name != "down":
+        if name == "down":
+            xs[name] = wl.linear_activations(M, 2 * K, cfg3["seed"] + i, cfg3["act_outlier_frac"],
+                                             cfg3["act_outlier_scale"])          # gate|up output stand-in
+        else:
             xs[name] = wl.linear_activations(M, K, cfg3["seed"] + i, cfg3["act_outlier_frac"],
-                                             cfg3["act_outlier_scale"])[:rows]
-    wq = {}
-    for i, (name, N, K) in enumerate(cfg3["linears"]):
-        wb = wl.linear_weights(N, K, cfg3["seed"] + 17 + 101 * i, cfg3["w_std"])[::nfrac]
-        wq[name] = oq.quantize_rows(wb)
+                                             cfg3["act_outlier_scale"])
+        wq[name] = oq.quantize_rows(wl.linear_weights(N // nfrac, K, cfg3["seed"] + 17 + 101 * i, cfg3["w_std"]))
     B, k, V, T = cfg4["B"], cfg4["k"], cfg4["V"], cfg4["temperature"]
     zt, zd = wl.accept_logits(B, k, V, cfg4["seed"], wl.C4_CORRELATION, scale=cfg4["logit_std"], rank=cfg4["rank"])
     x = wl.draft_tokens_sampled(zd, T, seed=cfg4["draft_seed"])
     u = wl.philox_uniforms((B, k + 1), seed=cfg4["uniform_seed"])
-    flops = 0.0
+    flops_rep = sum(2.0 * M * (N // nfrac) * K for _, N, K in cfg3["linears"])
+    reps = 0
     t0 = time.perf_counter()
-    gu = None
-    for name, N, K in cfg3["linears"]:
-        if name == "down":
-            inter = wq["gate_up"][0].shape[0] // 2
-            a, sa, _ = oq.quantize_silu_mul_rows(gu[:, :2 * inter])
-        else:
-            a, sa = oq.quantize_rows(xs[name])
-        w, sw = wq[name]
-        y = og.gemm(a, sa, w[:, :a.shape[1]], sw)
-        flops += 2.0 * a.shape[0] * w.shape[0] * a.shape[1]
-        if name == "gate_up":
-            gu = wl.bf16_bits_from_f32(y.astype(np.float32))
-    oa.accept_stochastic(zt[:bseq], zd[:bseq], x[:bseq], u[:bseq], T)
-    dt = time.perf_counter() - t0
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{rows} of {M} rows x every {nfrac}th output channel of the 4 layer linears "
-                      f"(quantize + exact fp64 GEMM + SiLU-gated re-quantize) and stochastic acceptance of "
-                      f"{bseq} of {B} sequences at V={V}; {dt:.2f} s"}
+    while True:
+        for name, N, K in cfg3["linears"]:
+            if name == "down":
+                a, sa, _ = oq.quantize_silu_mul_rows(xs[name])
+            else:
+                a, sa = oq.quantize_rows(xs[name])
+            w, sw = wq[name]
+            og.gemm(a, sa, w, sw)
+        oa.accept_stochastic(zt, zd, x, u, T)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds or reps >= max_reps:
+            break
+    return {"value": flops_rep * reps / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{reps}x: the 4 layer linears at M={M} on every {nfrac}th output channel (full K; "
+                      f"per-token and SiLU-gated quantize, exact fp64 GEMMs) plus stochastic acceptance of all "
+                      f"{B} sequences at V={V}; {dt:.1f} s"}
 
 
 def main(argv=None):
@@ -222,32 +219,46 @@ def main(argv=None):
     for i in range(args.warmup):
         step.run(weights[i % args.copies], logits[i % args.copies])
     torch.cuda.synchronize()
+
+    # The same step captured as a HIP graph per input copy (one replay
+    # launches all 12 kernels); reported beside the eager figure.
+    graphs = []
+    for c in range(args.copies):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step.run(weights[c], logits[c])
+        graphs.append(g)
+    for i in range(args.warmup):
+        graphs[i % args.copies].replay()
+    torch.cuda.synchronize()
     log("warmup done")
 
-    ev = {"gu": [], "acc": []}
-    evs = []
-    for i in range(args.steps):
-        e = {"gu": (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)),
-             "acc": (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))}
-        evs.append(e)
+    # timed region: K eager steps (launches queue ahead of the GPU)
     torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     t_start.record()
     for i in range(args.steps):
-        step.run(weights[i % args.copies], logits[i % args.copies], ev=evs[i])
+        step.run(weights[i % args.copies], logits[i % args.copies])
     t_end.record()
     torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_step = total_ms / args.steps
-    gu_us = float(np.mean([e["gu"][0].elapsed_time(e["gu"][1]) for e in evs])) * 1e3
-    acc_us = float(np.mean([e["acc"][0].elapsed_time(e["acc"][1]) for e in evs])) * 1e3
+    ms_step = t_start.elapsed_time(t_end) / args.steps
     num = step.num.cpu().numpy()
     tokens = float(np.sum(num + 1))
-    log(f"step {ms_step * 1e3:.1f} us; gate_up gemm {gu_us:.1f} us; accept {acc_us:.1f} us")
 
-    parts = time_parts(torch, step, weights, logits, reps=20)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        graphs[i % args.copies].replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step_graph = e0.elapsed_time(e1) / args.steps
+
+    parts = time_parts(torch, step, weights, logits, reps=22)
     gemm_us = parts["qkv"] + parts["o"] + parts["gate_up"] + parts["down"]
+    gu_us, acc_us = parts["gate_up"], parts["accept"]
+    log(f"step {ms_step * 1e3:.1f} us (eager), {ms_step_graph * 1e3:.1f} us (graph); gate_up gemm {gu_us:.1f} us; "
+        f"accept {acc_us:.1f} us")
 
     B, k, V = cfg4["B"], cfg4["k"], cfg4["V"]
     acc_bytes = 2.0 * B * (2 * k + 1) * V                       # target + draft logits read once
@@ -278,6 +289,7 @@ def main(argv=None):
             "verified_tokens_per_step": tokens,
             "verified_tokens_per_s_accept": round(tokens / (acc_us * 1e-6), 0),
             "verified_tokens_per_s_step": round(tokens / (ms_step * 1e-3), 0),
+            "ms_per_step_graph": round(ms_step_graph, 4),
         },
         "roofline": {
             "kernel": "gate|up FP8 GEMM (M=320, N=28672, K=4096)",
