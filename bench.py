@@ -21,6 +21,7 @@ are under "components".
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -188,6 +189,53 @@ def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=12):
                       f"{B} sequences at V={V}; {dt:.1f} s"}
 
 
+COPY_BYTES = 256 << 20
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_gate_up_M320_N28672_K4096_traffic.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2606_18502_amd", "csrc", "gemm.hip")
+
+
+def measured_traffic():
+    """HBM bytes per gate|up launch from the committed FETCH_SIZE/WRITE_SIZE
+    summary, or None when the GEMM source has changed since it was taken."""
+    try:
+        fields = {}
+        for line in open(TRAFFIC_PROFILE).read().splitlines():
+            if ":" in line:
+                key, val = line.split(":", 1)
+                fields[key.strip()] = val.split()[0] if val.split() else ""
+        digest = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+        if fields.get("gemm_source_sha256_16") != digest:
+            return None
+        return int(fields["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def profile_traffic(torch, p, wl):
+    """Kernels for the FETCH_SIZE / WRITE_SIZE passes: an elementwise copy that
+    reads and writes COPY_BYTES once (scales the counters to bytes), then three
+    launches of the gate|up GEMM on the benched shapes with the weights cold."""
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.add(src, 0.0, out=dst)                               # reads and writes COPY_BYTES
+    torch.cuda.synchronize()
+    cfg3 = wl.CONFIGS["C3"]
+    M = cfg3["M"]
+    _, N, K = [l for l in cfg3["linears"] if l[0] == "gate_up"][0]
+    a = torch.randint(0, 120, (M, K), dtype=torch.uint8, device="cuda")
+    sa = torch.rand(M, device="cuda") * 0.01 + 1e-3
+    ws = [torch.randint(0, 120, (N, K), dtype=torch.uint8, device="cuda") for _ in range(3)]
+    sw = torch.rand(N, device="cuda") * 0.01 + 1e-3
+    out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    wsb = torch.empty((max(p.gemm_workspace_bytes(M, N, K), 16),), dtype=torch.uint8, device="cuda")
+    for i in range(3):
+        p.gemm(a, sa, ws[i], sw, out=out, workspace=wsb)
+    torch.cuda.synchronize()
+    log("profile kernels done")
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -195,6 +243,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--copies", type=int, default=3, help="rotated copies of weights and logits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile", choices=["traffic"], default=None,
+                    help="for hardware-counter runs: a plain copy of 256 MiB (the counters' calibration), then "
+                         "3 launches of the gate|up GEMM, then exit")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}): the verify path runs on one "
@@ -210,6 +261,8 @@ def main(argv=None):
         return 2
     p.load_library()
     torch.cuda.set_device(0)
+    if args.profile == "traffic":
+        return profile_traffic(torch, p, wl)
     acts, weights, logits = build_inputs(torch, p, wl, args.copies)
     step = Step(torch, p, wl, acts)
     cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
@@ -297,7 +350,7 @@ def main(argv=None):
             "achieved": round(gu_bytes / (gu_us * 1e-6) / 1e9, 1),
             "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(gu_bytes / (gu_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 3),
-            "traffic": None,
+            "traffic": measured_traffic(),
             "algorithmic_bytes": gu_bytes,
             "avg_launch_us": round(gu_us, 2),
             "mfma_frac": round(gu_flops / (gu_us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 3),

@@ -91,29 +91,47 @@ struct GemmCfg {
 // 16 consecutive rows 16 different 16-byte bank groups.
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
+// Load group i (of kGroupsPerWave) of this wave for the stage at `stage`.
+template <class C>
+__device__ __forceinline__ void issue_group(const GemmArgs& g, char* stage, int m0, int n0, int64_t kbyte,
+                                            int wave, int lane, int i) {
+    const int r_in = lane >> 3;       // row within the 8-row group
+    const int slot = lane & 7;        // LDS slot this lane fills
+    const int grp = wave + i * C::kWaves;
+    const int row = grp * 8 + r_in;
+    const int chunk = slot ^ swz(row);   // logical 16-byte chunk loaded into it
+    const uint8_t* src;
+    if (row < C::BM) {
+        int m = m0 + row;
+        m = m < g.M ? m : g.M - 1;
+        src = g.a + (int64_t)m * g.lda + kbyte + chunk * 16;
+    } else {
+        int n = n0 + row - C::BM;
+        n = n < g.N ? n : g.N - 1;
+        src = g.w + (int64_t)n * g.ldw + kbyte + chunk * 16;
+    }
+    __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(stage + grp * 1024), 16, 0, 0);
+}
+
 template <class C>
 __device__ __forceinline__ void issue_stage(const GemmArgs& g, char* stage, int m0, int n0,
                                             int64_t kbyte, int wave, int lane) {
-    const int r_in = lane >> 3;       // row within the 8-row group
-    const int slot = lane & 7;        // LDS slot this lane fills
 #pragma unroll
-    for (int i = 0; i < C::kGroupsPerWave; ++i) {
-        const int grp = wave + i * C::kWaves;
-        const int row = grp * 8 + r_in;
-        const int chunk = slot ^ swz(row);   // logical 16-byte chunk loaded into it
-        const uint8_t* src;
-        if (row < C::BM) {
-            int m = m0 + row;
-            m = m < g.M ? m : g.M - 1;
-            src = g.a + (int64_t)m * g.lda + kbyte + chunk * 16;
-        } else {
-            int n = n0 + row - C::BM;
-            n = n < g.N ? n : g.N - 1;
-            src = g.w + (int64_t)n * g.ldw + kbyte + chunk * 16;
-        }
-        __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(stage + grp * 1024), 16, 0, 0);
-    }
+    for (int i = 0; i < C::kGroupsPerWave; ++i) issue_group<C>(g, stage, m0, n0, kbyte, wave, lane, i);
 }
+
+// Placement of the per-step work between the MFMAs of a K-step (numerators
+// over 8 of the step's MFMA count): the LDS reads of the next step are spread
+// over the first kReadSpan8/8 of the MFMAs, so they have completed by the end
+// of the step, and the stage refill loads over the first kLoadSpan8/8.
+#ifndef SPECFP8_READ_SPAN8
+#define SPECFP8_READ_SPAN8 5
+#endif
+#ifndef SPECFP8_LOAD_SPAN8
+#define SPECFP8_LOAD_SPAN8 4
+#endif
+constexpr int kReadSpan8 = SPECFP8_READ_SPAN8;
+constexpr int kLoadSpan8 = SPECFP8_LOAD_SPAN8;
 
 // vmcnt(N) with lgkmcnt/expcnt left alone (vmcnt field: bits [3:0] and [15:14]).
 template <int N>
@@ -195,25 +213,31 @@ __device__ __forceinline__ void kstep(const GemmArgs& g, char* const* stages, in
     wait_vmcnt<(STAGES - 2) * C::kGroupsPerWave>();
     __builtin_amdgcn_s_barrier();
     const int refill = min(it + STAGES, nk - 1);
-    issue_stage<C>(g, stages[S], m0, n0, (int64_t)(ks0 + (refill + krot) % nk) * kBK, wave, lane);
-    // MFMAs of step it, with the LDS reads of step it+1 spread between them so
-    // the LDS command queue never fills and blocks MFMA issue.  Each group is
-    // fenced with sched_barrier to keep this order.  On the last step the
-    // reads target the current stage (in bounds, results unused), which keeps
-    // the sequence free of branches.
+    const int64_t kref = (int64_t)(ks0 + (refill + krot) % nk) * kBK;
+    // MFMAs of step it, with the stage refill loads and the LDS reads of step
+    // it+1 spread between them so neither queue fills and blocks MFMA issue.
+    // Each group is fenced with sched_barrier to keep this order.  On the last
+    // step the reads target the current stage (in bounds, results unused),
+    // which keeps the sequence free of branches.
     const bool more = it + 1 < nk;
     const uint32_t st_next = lds_addr(stages[more ? (S + 1) % STAGES : S]);
     const int kg = lane >> 4;
     const int r16 = lane & 15;
     constexpr int kMfma = WTM * WTN;
     constexpr int kReads = 2 * (WTM + WTN);
+    constexpr int kG = C::kGroupsPerWave;
+    constexpr int kRSpan = (kMfma * kReadSpan8 + 7) / 8 > 0 ? (kMfma * kReadSpan8 + 7) / 8 : 1;
+    constexpr int kLSpan = (kMfma * kLoadSpan8 + 7) / 8 > 0 ? (kMfma * kLoadSpan8 + 7) / 8 : 1;
 #pragma unroll
     for (int t = 0; t < kMfma; ++t) {
         const int i = t / WTM, j = t % WTM;
+#pragma unroll
+        for (int q = 0; q < kG; ++q)
+            if ((q * kLSpan) / kG == t) issue_group<C>(g, stages[S], m0, n0, kref, wave, lane, q);
         acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(cur.w[i], cur.a[j], acc[i][j], 0, 0, 0, 0, 0, 0);
 #pragma unroll
         for (int r = 0; r < kReads; ++r) {
-            if ((r * kMfma) / kReads == t) {
+            if ((r * kRSpan) / kReads == t) {
                 const int f = r / 2, h = r & 1;
                 const int row = f < WTM ? (wm * WTM + f) * 16 + r16 : C::BM + (wn * WTN + f - WTM) * 16 + r16;
                 const u32x4 v = lds_half(st_next, row, 2 * kg + h);
@@ -231,6 +255,74 @@ __device__ __forceinline__ void kstep(const GemmArgs& g, char* const* stages, in
     for (int j = 0; j < WTM; ++j) asm volatile("" : "+v"(nxt.a[j]));
 #pragma unroll
     for (int i = 0; i < WTN; ++i) asm volatile("" : "+v"(nxt.w[i]));
+}
+
+template <int WTM, int WTN>
+__device__ __forceinline__ void load_scales(const GemmArgs& g, float (&sa_reg)[WTM], float (&sw_reg)[WTN][4], int m0,
+                                            int n0, int wm, int wn, int lane) {
+    const int kg0 = lane >> 4, r0 = lane & 15;
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) {
+        const int m = min(m0 + (wm * WTM + j) * 16 + r0, g.M - 1);
+        sa_reg[j] = g.a_per_tensor ? g.sa[0] : g.sa[m];
+    }
+#pragma unroll
+    for (int i = 0; i < WTN; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int n = min(n0 + (wn * WTN + i) * 16 + 4 * kg0 + r, g.N - 1);
+            sw_reg[i][r] = g.w_per_tensor ? g.sw[0] : g.sw[n];
+        }
+}
+
+// Epilogue: lane holds D[n = 4*(lane/16) + r][m = lane%16] of each 16x16
+// block; the scales were fetched into registers before the main loop.  With a
+// K split the fp32 partial goes to the workspace instead.
+template <int WTM, int WTN>
+__device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
+                                           const float (&sw_reg)[WTN][4], int m0, int n0, int wm, int wn, int lane,
+                                           int split) {
+    const int kg = lane >> 4;
+    const int r16 = lane & 15;
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) {
+        const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) {
+            const int m = m0 + (wm * WTM + j) * 16 + r16;
+            const v4f a = acc[i][j];
+            const bool ok = (n < g.N) && (m < g.M);
+            if (g.splits > 1) {
+                if (ok) {
+                    float* dst = g.partial + ((int64_t)split * g.M + m) * g.ldp + n;
+                    *reinterpret_cast<float4*>(dst) = make_float4(a[0], a[1], a[2], a[3]);
+                }
+                continue;
+            }
+            float y[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) y[r] = (a[r] * sa_reg[j]) * sw_reg[i][r];
+            if (!ok) continue;
+            if (g.out_f32) {
+                float* dst = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
+                if (n + 3 < g.N) {
+                    *reinterpret_cast<float4*>(dst) = make_float4(y[0], y[1], y[2], y[3]);
+                } else {
+                    for (int r = 0; r < 4 && n + r < g.N; ++r) dst[r] = y[r];
+                }
+            } else {
+                uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
+                if (n + 3 < g.N) {
+                    uint2 o;
+                    o.x = f32_to_bf16_rne(y[0]) | (f32_to_bf16_rne(y[1]) << 16);
+                    o.y = f32_to_bf16_rne(y[2]) | (f32_to_bf16_rne(y[3]) << 16);
+                    *reinterpret_cast<uint2*>(dst) = o;
+                } else {
+                    for (int r = 0; r < 4 && n + r < g.N; ++r) dst[r] = (uint16_t)f32_to_bf16_rne(y[r]);
+                }
+            }
+        }
+    }
 }
 
 template <int WTM, int WTN, int WM, int WN, int STAGES>
@@ -281,21 +373,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     // main loop (rows and columns past the edge read a valid neighbour).
     float sa_reg[WTM];
     float sw_reg[WTN][4];
-    {
-        const int kg0 = lane >> 4, r0 = lane & 15;
-#pragma unroll
-        for (int j = 0; j < WTM; ++j) {
-            const int m = min(m0 + (wm * WTM + j) * 16 + r0, g.M - 1);
-            sa_reg[j] = g.a_per_tensor ? g.sa[0] : g.sa[m];
-        }
-#pragma unroll
-        for (int i = 0; i < WTN; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int n = min(n0 + (wn * WTN + i) * 16 + 4 * kg0 + r, g.N - 1);
-                sw_reg[i][r] = g.w_per_tensor ? g.sw[0] : g.sw[n];
-            }
-    }
+    load_scales<WTM, WTN>(g, sa_reg, sw_reg, m0, n0, wm, wn, lane);
     Frags<WTM, WTN> f0, f1;
     wait_vmcnt<(STAGES - 1) * C::kGroupsPerWave>();
     __builtin_amdgcn_s_barrier();
@@ -332,49 +410,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
 #undef SPEC_STEP
     wait_vmcnt<0>();   // no direct-to-LDS write may outlive the workgroup
 
-    const int kg = lane >> 4;
-    const int r16 = lane & 15;
-    // epilogue: lane holds D[n = 4*(lane/16) + r][m = lane%16] of each 16x16
-    // block; the scales were fetched into registers before the main loop.
-#pragma unroll
-    for (int i = 0; i < WTN; ++i) {
-        const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
-#pragma unroll
-        for (int j = 0; j < WTM; ++j) {
-            const int m = m0 + (wm * WTM + j) * 16 + r16;
-            const v4f a = acc[i][j];
-            const bool ok = (n < g.N) && (m < g.M);
-            if (g.splits > 1) {
-                if (ok) {
-                    float* dst = g.partial + ((int64_t)split * g.M + m) * g.ldp + n;
-                    *reinterpret_cast<float4*>(dst) = make_float4(a[0], a[1], a[2], a[3]);
-                }
-                continue;
-            }
-            float y[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) y[r] = (a[r] * sa_reg[j]) * sw_reg[i][r];
-            if (!ok) continue;
-            if (g.out_f32) {
-                float* dst = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-                if (n + 3 < g.N) {
-                    *reinterpret_cast<float4*>(dst) = make_float4(y[0], y[1], y[2], y[3]);
-                } else {
-                    for (int r = 0; r < 4 && n + r < g.N; ++r) dst[r] = y[r];
-                }
-            } else {
-                uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-                if (n + 3 < g.N) {
-                    uint2 o;
-                    o.x = f32_to_bf16_rne(y[0]) | (f32_to_bf16_rne(y[1]) << 16);
-                    o.y = f32_to_bf16_rne(y[2]) | (f32_to_bf16_rne(y[3]) << 16);
-                    *reinterpret_cast<uint2*>(dst) = o;
-                } else {
-                    for (int r = 0; r < 4 && n + r < g.N; ++r) dst[r] = (uint16_t)f32_to_bf16_rne(y[r]);
-                }
-            }
-        }
-    }
+    store_tile<WTM, WTN>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split);
 }
 
 // Sum the split-K partials in split order, then scale and convert.
@@ -441,9 +477,8 @@ constexpr int kCfgBN[8] = {Cfg0::BN, Cfg1::BN, Cfg2::BN, Cfg3::BN, Cfg4::BN, Cfg
 
 template <class C, int WTM, int WTN, int WM, int WN, int STAGES>
 hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
-    auto kern = gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES>;
     const int total = g.m_tiles * g.n_tiles * g.splits;
-    hipLaunchKernelGGL(kern, dim3(total), dim3(C::kThreads), 0, stream, g);
+    hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES>), dim3(total), dim3(C::kThreads), 0, stream, g);
     return hipGetLastError();
 }
 
