@@ -52,7 +52,9 @@ typedef enum {
 typedef enum {
     SPEC_SCALE_PER_ROW = 0,    /* dynamic: one scale per row (per token for activations,
                                   per output channel for weights W[N,K])              */
-    SPEC_SCALE_PER_TENSOR = 1  /* static: one fp32 scale for the whole tensor         */
+    SPEC_SCALE_PER_TENSOR = 1, /* static: one fp32 scale for the whole tensor         */
+    SPEC_SCALE_CALIBRATE = 2   /* spec_fp8_quantize only: fold the tensor's scale into a
+                                  running static scale (min-max calibration)          */
 } spec_scale_mode;
 
 typedef enum {
@@ -79,6 +81,15 @@ typedef enum {
  *   PER_ROW:    s[r] = max(fl32(max_c |v[c]| / 448), 2^-100); scales[r] = s[r]   (written)
  *   PER_TENSOR: s[r] = scales[0]                                               (read)
  *   q[r,c] = E4M3(fl32(v[c] * fl32(1 / s[r])))
+ *   CALIBRATE:  scales[0] = max(scales[0], max_r s[r]) with s[r] as for PER_ROW;
+ *               nothing else is written (q may be NULL; ld_q is not checked).
+ *               This is the static min-max calibration of section 3.2: because
+ *               fl32(a/448) is monotone in a, the max of the row scales over all
+ *               calibration batches equals the scale of the largest magnitude
+ *               seen.  The caller sets scales[0] to 0 (or a previous running
+ *               value, finite and >= 0) before the first batch; the update is
+ *               an atomic max, so the result does not depend on the order of
+ *               rows or of calls.
  *
  * E4M3(.) rounds to nearest with ties to the even mantissa and saturates any
  * magnitude above 448 to +-448; NaN gives 0x7F; the sign of zero is kept.
@@ -88,8 +99,8 @@ typedef enum {
  * from an exact evaluation by one bf16 ulp at near-ties of its rounding.
  *
  * x       bf16 [rows, ld_x]; cols (or 2*cols for SILU_MUL) <= ld_x.
- * scales  fp32 [rows] (PER_ROW, written) or fp32 [1] (PER_TENSOR, read; must be
- *         finite and > 0).
+ * scales  fp32 [rows] (PER_ROW, written), fp32 [1] (PER_TENSOR, read; must be
+ *         finite and > 0) or fp32 [1] (CALIBRATE, read and updated).
  * q       uint8 [rows, ld_q], cols <= ld_q.
  * Requirements: rows >= 0 (0 is a no-op), cols > 0 and cols % 8 == 0,
  * ld_x % 8 == 0, ld_q % 8 == 0, x and q 16-byte aligned (SPEC_ERR_ALIGN or

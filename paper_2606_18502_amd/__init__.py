@@ -13,6 +13,7 @@ include/spec_fp8.h); this package only marshals torch tensors into that ABI.
 from ._lib import SpecError, load as load_library, LIB_PATH  # noqa: F401
 from .ops import (  # noqa: F401
     quantize,
+    calibrate,
     silu_mul,
     gemm,
     gemm_workspace_bytes,

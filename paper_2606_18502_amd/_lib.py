@@ -13,7 +13,7 @@ SPEC_OK = 0
 STATUS_NAMES = {0: "SPEC_OK", 1: "SPEC_ERR_NULL", 2: "SPEC_ERR_SHAPE", 3: "SPEC_ERR_UNSUPPORTED",
                 4: "SPEC_ERR_ENUM", 5: "SPEC_ERR_ALIGN", 6: "SPEC_ERR_WORKSPACE", 7: "SPEC_ERR_HIP",
                 8: "SPEC_ERR_VALUE"}
-SCALE_PER_ROW, SCALE_PER_TENSOR = 0, 1
+SCALE_PER_ROW, SCALE_PER_TENSOR, SCALE_CALIBRATE = 0, 1, 2
 QIN_BF16, QIN_SILU_MUL_BF16 = 0, 1
 OUT_BF16, OUT_F32 = 0, 1
 

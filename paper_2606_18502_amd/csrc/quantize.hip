@@ -62,6 +62,14 @@ __device__ __forceinline__ void row_scale(float amax, float* s_out, float* inv_o
     *inv_out = (float)(1.0 / (double)s);
 }
 
+// Static calibration: running[0] = max(running[0], s).  Scales are finite and
+// non-negative, and the bit patterns of non-negative floats order like
+// unsigned integers, so an integer atomic max is exact and order-independent.
+__device__ __forceinline__ void calibrate_max(float* running, float s) {
+    atomicMax(reinterpret_cast<unsigned int*>(running), __float_as_uint(s));
+}
+
+// MODE 0: per-row scales (written); 1: one given scale; 2: calibration only.
 // NCH > 0: the row lives in registers (NCH chunks of 8 per thread).
 // NCH == 0: rows too wide for registers; amax pass and encode pass each read the row.
 template <int IN_KIND, int MODE, int NCH>
@@ -89,6 +97,12 @@ __global__ __launch_bounds__(kQMaxThreads) void quantize_rows_kernel(
             }
         }
         float s, inv;
+        if (MODE == 2) {
+            amax = block_max(amax, red);
+            row_scale(amax, &s, &inv);
+            if (t == 0) calibrate_max(scales, s);
+            return;
+        }
         if (MODE == 0) {
             amax = block_max(amax, red);
             row_scale(amax, &s, &inv);
@@ -104,7 +118,7 @@ __global__ __launch_bounds__(kQMaxThreads) void quantize_rows_kernel(
         }
     } else {
         float s, inv;
-        if (MODE == 0) {
+        if (MODE != 1) {
             float amax = 0.0f;
             for (int64_t c = t; c < nchunks; c += nt) {
                 float v[8];
@@ -114,6 +128,10 @@ __global__ __launch_bounds__(kQMaxThreads) void quantize_rows_kernel(
             }
             amax = block_max(amax, red);
             row_scale(amax, &s, &inv);
+            if (MODE == 2) {
+                if (t == 0) calibrate_max(scales, s);
+                return;
+            }
             if (t == 0) scales[row] = s;
         } else {
             s = scales[0];
@@ -186,8 +204,12 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t cols, int64_
         return launch_quantize_t<0, 0>(x, rows, cols, ld_x, scales, q, ld_q, stream);
     if (in_kind == 0 && mode == 1)
         return launch_quantize_t<0, 1>(x, rows, cols, ld_x, scales, q, ld_q, stream);
+    if (in_kind == 0 && mode == 2)
+        return launch_quantize_t<0, 2>(x, rows, cols, ld_x, scales, q, ld_q, stream);
     if (in_kind == 1 && mode == 0)
         return launch_quantize_t<1, 0>(x, rows, cols, ld_x, scales, q, ld_q, stream);
+    if (in_kind == 1 && mode == 2)
+        return launch_quantize_t<1, 2>(x, rows, cols, ld_x, scales, q, ld_q, stream);
     return launch_quantize_t<1, 1>(x, rows, cols, ld_x, scales, q, ld_q, stream);
 }
 

@@ -16,15 +16,18 @@ constexpr int64_t kMaxGridY = 65535;       // grid.y limit
 spec_status check_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, int in_kind, int mode,
                            const float* scales, const void* q, int64_t ld_q) {
     if (in_kind != SPEC_QIN_BF16 && in_kind != SPEC_QIN_SILU_MUL_BF16) return SPEC_ERR_ENUM;
-    if (mode != SPEC_SCALE_PER_ROW && mode != SPEC_SCALE_PER_TENSOR) return SPEC_ERR_ENUM;
+    if (mode != SPEC_SCALE_PER_ROW && mode != SPEC_SCALE_PER_TENSOR && mode != SPEC_SCALE_CALIBRATE)
+        return SPEC_ERR_ENUM;
+    const bool codes = mode != SPEC_SCALE_CALIBRATE;   // calibration writes no codes
     if (rows < 0 || cols <= 0) return SPEC_ERR_SHAPE;
     const int64_t in_cols = in_kind == SPEC_QIN_SILU_MUL_BF16 ? 2 * cols : cols;
-    if (ld_x < in_cols || ld_q < cols) return SPEC_ERR_SHAPE;
+    if (ld_x < in_cols || (codes && ld_q < cols)) return SPEC_ERR_SHAPE;
     if (rows > kMaxGrid) return SPEC_ERR_UNSUPPORTED;
     if (cols % 8 != 0) return SPEC_ERR_UNSUPPORTED;
     if (rows == 0) return SPEC_OK;
-    if (!x || !q || !scales) return SPEC_ERR_NULL;
-    if (ld_x % 8 != 0 || ld_q % 8 != 0 || !aligned16(x) || !aligned16(q)) return SPEC_ERR_ALIGN;
+    if (!x || (codes && !q) || !scales) return SPEC_ERR_NULL;
+    if (ld_x % 8 != 0 || !aligned16(x)) return SPEC_ERR_ALIGN;
+    if (codes && (ld_q % 8 != 0 || !aligned16(q))) return SPEC_ERR_ALIGN;
     if ((reinterpret_cast<uintptr_t>(scales) & 3u) != 0) return SPEC_ERR_ALIGN;
     return SPEC_OK;
 }

@@ -66,6 +66,26 @@ def quantize(x: torch.Tensor, per_tensor_scale: Optional[torch.Tensor] = None, s
     return out, scales
 
 
+def calibrate(x: torch.Tensor, running_scale: torch.Tensor, silu_mul: bool = False) -> torch.Tensor:
+    """Static min-max calibration step (spec_fp8_quantize, SPEC_SCALE_CALIBRATE).
+
+    running_scale: fp32 [1], updated in place to max(running_scale, scale of
+    the largest |x|); start it at 0 and pass every calibration batch.
+    """
+    lib = _lib.load()
+    _dev(x, torch.bfloat16, "x")
+    _dev(running_scale, torch.float32, "running_scale")
+    if running_scale.numel() != 1:
+        raise ValueError("running_scale must hold one fp32 value")
+    rows = x.shape[0]
+    cols = x.shape[1] // 2 if silu_mul else x.shape[1]
+    kind = _lib.QIN_SILU_MUL_BF16 if silu_mul else _lib.QIN_BF16
+    check("spec_fp8_quantize", lib.spec_fp8_quantize(x.data_ptr(), rows, cols, _rowmajor(x, "x"), kind,
+                                                     _lib.SCALE_CALIBRATE, running_scale.data_ptr(), None, 0,
+                                                     _stream()))
+    return running_scale
+
+
 def silu_mul(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """h = bf16(silu(gate) * up) for x = [gate | up] bf16 [rows, 2*cols] (spec_silu_mul_bf16)."""
     lib = _lib.load()

@@ -67,6 +67,13 @@ def test_quantize_validation(lib):
     assert q(lib, ld_x=68) == ALIGN
     assert q(lib, scales=A16 + 2) == ALIGN
     assert q(lib, rows=0, x=None, scales=None, qp=None) == OK   # empty: no-op
+    # static calibration writes no codes: q and ld_q are not checked
+    assert q(lib, mode=3) == ENUM
+    assert q(lib, mode=2, rows=0, qp=None, ld_q=0) == OK
+    assert q(lib, mode=2, x=None, qp=None, ld_q=0) == NULL
+    assert q(lib, mode=2, scales=None, qp=None, ld_q=0) == NULL
+    assert q(lib, mode=2, x=A1, qp=None, ld_q=0) == ALIGN
+    assert q(lib, mode=2, ld_x=32, qp=None, ld_q=0) == SHAPE
 
 
 def test_silu_mul_validation(lib):
@@ -85,6 +92,8 @@ def g(lib, a=A16, lda=512, sa=A16, am=0, w=A16, ldw=512, sw=A16, wm=0, M=8, N=10
 
 def test_gemm_validation(lib):
     assert g(lib, am=3) == ENUM
+    assert g(lib, am=2) == ENUM        # calibration is a quantize mode only
+    assert g(lib, wm=2) == ENUM
     assert g(lib, wm=-1) == ENUM
     assert g(lib, od=7) == ENUM
     assert g(lib, M=-1) == SHAPE

@@ -122,6 +122,38 @@ def test_per_tensor_from_calibration_matches_row_scales():
     assert np.float32(max(s.max() for s in srow)) == oq.calibrate_per_tensor(batches)
 
 
+@pytest.mark.parametrize("cols", [512, 4096, 65536 + 512])     # registers, and the two-pass wide-row path
+def test_calibrate_mode_bit_exact(cols):
+    """SPEC_SCALE_CALIBRATE folds every batch into the running scale: equal
+    to the oracle's min-max calibration bit for bit, also when the running
+    value starts above the batches' own maximum (it must then stay put)."""
+    p = need_gpu()
+    batches = [wl.student_t_activations(rows, cols, seed=300 + i) for i, rows in enumerate((3, 17, 64, 1))]
+    running = torch.zeros(1, dtype=torch.float32, device="cuda")
+    for b in batches:
+        p.calibrate(dev_bf16(b), running)
+    ref = oq.calibrate_per_tensor(batches)
+    assert host(running)[0].tobytes() == np.float32(ref).tobytes()
+    big = torch.full((1,), float(ref) * 2.0, dtype=torch.float32, device="cuda")
+    p.calibrate(dev_bf16(batches[0]), big)
+    assert host(big)[0] == np.float32(float(ref) * 2.0)
+    zero = torch.zeros(1, dtype=torch.float32, device="cuda")
+    p.calibrate(dev_bf16(np.zeros((4, cols), np.uint16)), zero)      # all-zero rows: the scale floor 2^-100
+    assert host(zero)[0] == np.float32(2.0 ** -100)
+
+
+def test_calibrate_silu_mul_input():
+    """Calibration of the SiLU-gated FFN input uses the same intermediate h
+    as the fused quantize, so its scale equals the max of that path's row scales."""
+    p = need_gpu()
+    xb = wl.gated_ffn_input(40, 1024, seed=17)
+    x = dev_bf16(xb)
+    _, srow = p.quantize(x, silu_mul=True)
+    running = torch.zeros(1, dtype=torch.float32, device="cuda")
+    p.calibrate(x, running, silu_mul=True)
+    assert host(running)[0] == host(srow).max()
+
+
 def test_deterministic():
     p = need_gpu()
     xb = wl.linear_activations(64, 4096, 11, outlier_frac=0.005, outlier_scale=30.0)
