@@ -139,7 +139,34 @@ def time_parts(torch, step, weights, logits, reps):
     return res
 
 
-def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=12):
+def vendor_gemm(torch, step, weights, reps=22):
+    """The same four GEMMs through hipBLASLt (torch._scaled_mm on the same
+    E4M3 codes, per-row activation and per-channel weight scales, bf16 out),
+    timed like time_parts: a reference point from the vendor library, not
+    part of the path.  None where the library refuses the call."""
+    f8 = torch.float8_e4m3fn
+    res = {}
+    for n in ("qkv", "o", "gate_up", "down"):
+        try:
+            a = step.q[n].view(f8)
+            sa = step.s[n].view(-1, 1)
+            evs = []
+            for r in range(reps):
+                w, sw = weights[r % len(weights)][n]
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                torch._scaled_mm(a, w.view(f8).t(), scale_a=sa, scale_b=sw.view(1, -1), out_dtype=torch.bfloat16)
+                e1.record()
+                evs.append((e0, e1))
+            torch.cuda.synchronize()
+            res[n] = round(float(np.mean([x.elapsed_time(y) for x, y in evs[2:]])) * 1e3, 1)
+        except Exception as e:      # a library without this FP8 path
+            log(f"hipBLASLt {n}: {str(e)[:100]}")
+            res[n] = None
+    return res
+
+
+def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40):
     """The oracle on the host cores, on a bounded sample of the benched step:
     the 4 linears at M=320 restricted to every `nfrac`-th output channel
     (full K; per-token quantize, the SiLU-gated re-quantize of a full-width
@@ -308,6 +335,7 @@ def main(argv=None):
     ms_step_graph = e0.elapsed_time(e1) / args.steps
 
     parts = time_parts(torch, step, weights, logits, reps=22)
+    vendor = vendor_gemm(torch, step, weights)
     gemm_us = parts["qkv"] + parts["o"] + parts["gate_up"] + parts["down"]
     gu_us, acc_us = parts["gate_up"], parts["accept"]
     log(f"step {ms_step * 1e3:.1f} us (eager), {ms_step_graph * 1e3:.1f} us (graph); gate_up gemm {gu_us:.1f} us; "
@@ -336,6 +364,7 @@ def main(argv=None):
             "gemm_only_tflops": round(gemm_flops / (gemm_us * 1e-6) / 1e12, 1),
             "gemm_only_pct_mfma_peak": round(100 * gemm_flops / (gemm_us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 1),
             "gemm_us": {n: round(parts[n], 1) for n in ("qkv", "o", "gate_up", "down")},
+            "hipblaslt_gemm_us": vendor,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),

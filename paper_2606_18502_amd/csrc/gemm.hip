@@ -463,6 +463,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g) {
 //  5   160 x 128  2x2 (80x64)           4       144 KiB  M <= 320
 //  6   320 x 64   4x1 (80x64)           3       144 KiB
 //  7   160 x 64   2x2 (80x32)           4       112 KiB
+//  8    64 x 128  2x2 (32x64)           4        96 KiB   M <= 320, short N (QKV, O)
 using Cfg0 = GemmCfg<2, 2, 2, 2, 4>;
 using Cfg1 = GemmCfg<5, 4, 1, 2, 4>;
 using Cfg2 = GemmCfg<5, 7, 2, 2, 3>;
@@ -471,9 +472,11 @@ using Cfg4 = GemmCfg<5, 6, 2, 2, 3>;
 using Cfg5 = GemmCfg<5, 4, 2, 2, 4>;
 using Cfg6 = GemmCfg<5, 4, 4, 1, 3>;
 using Cfg7 = GemmCfg<5, 2, 2, 2, 4>;
+using Cfg8 = GemmCfg<2, 4, 2, 2, 4>;
+constexpr int kKinds = 9;
 
-constexpr int kCfgBM[8] = {Cfg0::BM, Cfg1::BM, Cfg2::BM, Cfg3::BM, Cfg4::BM, Cfg5::BM, Cfg6::BM, Cfg7::BM};
-constexpr int kCfgBN[8] = {Cfg0::BN, Cfg1::BN, Cfg2::BN, Cfg3::BN, Cfg4::BN, Cfg5::BN, Cfg6::BN, Cfg7::BN};
+constexpr int kCfgBM[kKinds] = {Cfg0::BM, Cfg1::BM, Cfg2::BM, Cfg3::BM, Cfg4::BM, Cfg5::BM, Cfg6::BM, Cfg7::BM, Cfg8::BM};
+constexpr int kCfgBN[kKinds] = {Cfg0::BN, Cfg1::BN, Cfg2::BN, Cfg3::BN, Cfg4::BN, Cfg5::BN, Cfg6::BN, Cfg7::BN, Cfg8::BN};
 
 template <class C, int WTM, int WTN, int WM, int WN, int STAGES>
 hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
@@ -490,11 +493,12 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
     //   M <= 64: 64x64;  M <= 80: 80x128;
     //   M <= 320: 160x224 when N fills >= 64 such columns exactly (gate|up),
     //             160x128 with a K split for long-K layers (down), else
-    //             160x64 (QKV, O: more tiles, no split);
+    //             64x128 (QKV, O: a CU's time is set by the operand rows it
+    //             streams per K-step, 192 here against 224 for 160x64);
     //   larger M: 160x224.
     if (M <= 64) p.kind = 0;
     else if (M <= 80) p.kind = 1;
-    else if (M <= 320) p.kind = (N % 224 == 0 && N >= 224 * 64) ? 2 : (K >= 2 * N ? 5 : 7);
+    else if (M <= 320) p.kind = (N % 224 == 0 && N >= 224 * 64) ? 2 : (K >= 2 * N ? 5 : 8);
     else p.kind = 2;
     const int ksteps = (int)(K / kBK);
     int splits = 0;
@@ -502,7 +506,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
     // tuning builds only: SPECFP8_GEMM_PLAN="kind:splits" overrides the choice
     if (const char* env = getenv("SPECFP8_GEMM_PLAN")) {
         int k = -1, sp = 0;
-        if (sscanf(env, "%d:%d", &k, &sp) >= 1 && k >= 0 && k < 8) { p.kind = k; splits = sp; }
+        if (sscanf(env, "%d:%d", &k, &sp) >= 1 && k >= 0 && k < kKinds) { p.kind = k; splits = sp; }
     }
 #endif
     const int bm = kCfgBM[p.kind], bn = kCfgBN[p.kind];
@@ -549,7 +553,8 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
         case 4: e = launch_cfg<Cfg4, 5, 6, 2, 2, 3>(g, stream); break;
         case 5: e = launch_cfg<Cfg5, 5, 4, 2, 2, 4>(g, stream); break;
         case 6: e = launch_cfg<Cfg6, 5, 4, 4, 1, 3>(g, stream); break;
-        default: e = launch_cfg<Cfg7, 5, 2, 2, 2, 4>(g, stream); break;
+        case 7: e = launch_cfg<Cfg7, 5, 2, 2, 2, 4>(g, stream); break;
+        default: e = launch_cfg<Cfg8, 2, 4, 2, 2, 4>(g, stream); break;
     }
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t work = M * ((N + 3) / 4);

@@ -54,6 +54,7 @@ def _sample(n, count, seed):
     (1, 16, 128), (17, 100, 256), (64, 64, 128),           # small tile, ragged
     (80, 1040, 512), (100, 4096, 1024),                    # 80-row tile, split-K
     (320, 640, 4096), (333, 272, 2048),                    # 320-row tile, split-K, ragged M
+    (300, 1000, 1024),                                     # 64x128 tile, ragged M and N, split-K
     (700, 400, 512), (1024, 1024, 1024),                   # 256-row tile
 ])
 def test_gemm_parity(M, N, K):
