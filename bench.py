@@ -116,10 +116,11 @@ def time_parts(torch, step, weights, logits, reps):
     """Per-part event timing: each part (one GEMM, or the acceptance) is
     launched `reps` times back to back on the current stream, every launch
     bracketed by HIP events, so the GPU never waits for the host between
-    them; returns the mean launch duration in us per part."""
+    them; returns the mean launch duration in us per part, and the 10th and
+    90th percentiles."""
     p = step.p
     names = ["qkv", "o", "gate_up", "down", "accept"]
-    res = {}
+    res, spread = {}, {}
     for n in names:
         evs = []
         for r in range(reps):
@@ -135,8 +136,10 @@ def time_parts(torch, step, weights, logits, reps):
             e1.record()
             evs.append((e0, e1))
         torch.cuda.synchronize()
-        res[n] = float(np.mean([a.elapsed_time(b) for a, b in evs[2:]])) * 1e3
-    return res
+        ts = np.array([a.elapsed_time(b) for a, b in evs[2:]]) * 1e3
+        res[n] = float(np.mean(ts))
+        spread[n] = [round(float(np.percentile(ts, 10)), 1), round(float(np.percentile(ts, 90)), 1)]
+    return res, spread
 
 
 def vendor_gemm(torch, step, weights, reps=22):
@@ -334,7 +337,7 @@ def main(argv=None):
     torch.cuda.synchronize()
     ms_step_graph = e0.elapsed_time(e1) / args.steps
 
-    parts = time_parts(torch, step, weights, logits, reps=22)
+    parts, spread = time_parts(torch, step, weights, logits, reps=22)
     vendor = vendor_gemm(torch, step, weights)
     gemm_us = parts["qkv"] + parts["o"] + parts["gate_up"] + parts["down"]
     gu_us, acc_us = parts["gate_up"], parts["accept"]
@@ -365,6 +368,7 @@ def main(argv=None):
             "gemm_only_pct_mfma_peak": round(100 * gemm_flops / (gemm_us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 1),
             "gemm_us": {n: round(parts[n], 1) for n in ("qkv", "o", "gate_up", "down")},
             "hipblaslt_gemm_us": vendor,
+            "part_us_p10_p90": spread,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),
@@ -372,6 +376,10 @@ def main(argv=None):
             "verified_tokens_per_s_accept": round(tokens / (acc_us * 1e-6), 0),
             "verified_tokens_per_s_step": round(tokens / (ms_step * 1e-3), 0),
             "ms_per_step_graph": round(ms_step_graph, 4),
+            # projection, not a measurement: 40 layers (target 32 + drafter 8) of these linears and
+            # quantizes plus one acceptance; attention, norms and the LM head are not included
+            "projected_tokens_per_s_40_layers": round(
+                tokens / ((40 * (ms_step * 1e3 - acc_us) + acc_us) * 1e-6), 0),
         },
         "roofline": {
             "kernel": "gate|up FP8 GEMM (M=320, N=28672, K=4096)",
