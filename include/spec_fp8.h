@@ -146,6 +146,44 @@ spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, s
                           void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * spec_fp8_gemm_logit_stats -- the LM-head projection of the verify pass (the
+ * target model's output layer over the M = B*(k+1) verify rows, hidden size K
+ * to vocabulary V; section 3.1) as an FP8 GEMM whose epilogue also produces
+ * the acceptance statistics of the logits it writes, so that the acceptance
+ * test does not read the target logits a second time for them.
+ *
+ *   z[m,n] = bf16_RNE(fl32(fl32(acc[m,n] * sa(m)) * sw(n)))   -- spec_fp8_gemm,
+ *            bf16 out, except that K is never split here (where spec_fp8_gemm
+ *            splits K for this shape the fp32 summation order differs)
+ *   for every row m and column group c, 0 <= c < spec_logit_stats_count(M, V, K)
+ *   (a group is a contiguous range of columns; the groups, in column order,
+ *   partition [0, V); a group may be empty):
+ *     temperature > 0:  c2 = fl32(log2(e) / T),
+ *                       Mc = fl32(max_{n in c} z[m,n] * c2),
+ *                       Zc = sum_{n in c} 2^fl32(fma(z[m,n], c2, -Mc))   (fp32, order unspecified)
+ *                       stats[m,c] = (Mc, Zc); an empty group is (-inf, 0)
+ *     temperature == 0: stats[m,c] = (max_{n in c} z[m,n], lowest n attaining it as int32 bits);
+ *                       an empty group is (-inf, INT32_MAX as int32 bits)
+ *   so that max_c Mc and sum_c Zc * 2^(Mc - max) are the row's softmax maximum
+ *   and normalizer of z/T in base 2 (the first pass of the acceptance test), and
+ *   the best (value, lowest index) pair is the row's argmax (T == 0).
+ *
+ * a, lda, a_scale, a_mode, w, ldw, w_scale, w_mode, M, K: as spec_fp8_gemm with N = V.
+ * logits  bf16 [M, ld_logits]; V <= ld_logits, ld_logits % 8 == 0, 16-byte aligned.
+ * stats   pairs of fp32 [M, ld_stats] (ld_stats counted in pairs, >= the group
+ *         count), 8-byte aligned.
+ * temperature finite and >= 0 (SPEC_ERR_VALUE otherwise).  No workspace.
+ * spec_logit_stats_count returns 0 for arguments spec_fp8_gemm would reject.
+ */
+size_t spec_logit_stats_count(int64_t M, int64_t V, int64_t K);
+
+spec_status spec_fp8_gemm_logit_stats(const uint8_t* a, int64_t lda, const float* a_scale, spec_scale_mode a_mode,
+                                      const uint8_t* w, int64_t ldw, const float* w_scale, spec_scale_mode w_mode,
+                                      int64_t M, int64_t V, int64_t K, float temperature,
+                                      void* logits, int64_t ld_logits, float* stats, int64_t ld_stats,
+                                      void* stream);
+
+/*
  * spec_verify_accept -- acceptance of B drafted chains of length k
  * (section 3.1; the rule of the speculative-sampling papers it cites):
  *
@@ -181,6 +219,28 @@ spec_status spec_verify_accept(const void* target_logits, const void* draft_logi
                                int64_t B, int64_t k, int64_t V, float temperature,
                                int32_t* out_tokens, int32_t* num_accepted,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * spec_verify_accept_stats -- spec_verify_accept with the target rows'
+ * statistics taken from spec_fp8_gemm_logit_stats (called with the same
+ * temperature on the rows of target_logits) instead of computed from
+ * target_logits: only draft_logits, when given, are streamed for theirs, and
+ * target_logits are read only at the draft tokens and in the row of the
+ * sampled position.
+ *
+ * target_stats  pairs of fp32 [B*(k+1), ld_stats], row i*(k+1)+p for sequence i,
+ *               position p (the row order of target_logits); n_stats entries per row,
+ *               1 <= n_stats <= ld_stats, n_stats < 2^31; 8-byte aligned.
+ * All other arguments, requirements, workspace and results as spec_verify_accept.
+ * The results equal spec_verify_accept's except for a decision within the fp32
+ * rounding of the statistics of its boundary (their summation order differs).
+ */
+spec_status spec_verify_accept_stats(const void* target_logits, const float* target_stats,
+                                     int64_t n_stats, int64_t ld_stats, const void* draft_logits,
+                                     const int32_t* draft_tokens, const float* uniforms,
+                                     int64_t B, int64_t k, int64_t V, float temperature,
+                                     int32_t* out_tokens, int32_t* num_accepted,
+                                     void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static description of a status code (never NULL). */
 const char* spec_status_string(spec_status s);

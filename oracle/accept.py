@@ -87,6 +87,18 @@ def softmax64(z_bits_row: np.ndarray, temperature: float) -> np.ndarray:
     return e / np.sum(e)
 
 
+def softmax_normalizer(z_bits: np.ndarray, temperature: float):
+    """The two numbers the first pass of speculative sampling needs per logit
+    row (the softmax of section 3.1's acceptance rule, p = softmax(z / T)):
+    the largest logit zmax and Z = sum_v exp((z_v - zmax) / T), so that
+    p_v = exp((z_v - zmax) / T) / Z.  fp64, rows along the last axis; T is
+    taken as the fp32 value passed.  Returns (zmax [...], Z [...])."""
+    z = bf16_to_f32(z_bits).astype(np.float64)
+    zmax = np.max(z, axis=-1)
+    Z = np.sum(np.exp((z - zmax[..., None]) / float(np.float32(temperature))), axis=-1)
+    return zmax, Z
+
+
 def _residual(p, q, x, V):
     """r = max(0, p - q); with q None (one-hot at x) that is p with r[x] = 0."""
     if q is None:

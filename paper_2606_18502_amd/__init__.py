@@ -17,6 +17,8 @@ from .ops import (  # noqa: F401
     silu_mul,
     gemm,
     gemm_workspace_bytes,
+    gemm_logit_stats,
+    logit_stats_count,
     verify_accept,
     accept_workspace_bytes,
 )

@@ -48,16 +48,32 @@ struct AcceptArgs {
     const float* u;
     int32_t* out;
     int32_t* num;
-    float2* stats;         // [B][R][nslice]
+    float2* stats;         // [B][Rs][nslice] statistics of the streamed rows
+    const float2* tst;     // target rows' statistics from the LM-head epilogue, or null
+    int64_t ldtst;         // row stride of tst (entries)
+    uint32_t ntst;         // entries per target row in tst
     double* chunkm;        // [B][nchunk] residual mass per chunk
     double* finem;         // [B][nchunk][256] residual mass per 64-element range
     unsigned int* ctr;     // [B]
     int64_t V, nchunk;
     uint32_t nslice, items;   // slices per row; rows * nslice (< 2^31)
     int B, k;
-    uint32_t R;            // rows per sequence in `stats`
+    uint32_t R;            // rows per sequence whose statistics are merged (k+1, or 2k+1 with draft logits)
+    uint32_t Rs;           // of these, the rows the statistics kernel streams (R, or R - (k+1) with tst)
+    uint32_t rt0;          // first streamed row within the sequence (0, or k+1 with tst)
     float c2;              // log2(e) / T
 };
+
+// Statistics entries of row r (0..R-1) of sequence b: the target rows from
+// the LM-head epilogue when given, else (and for draft rows) the streamed ones.
+__device__ __forceinline__ const float2* row_stats(const AcceptArgs& a, int b, int r, uint32_t& n) {
+    if ((uint32_t)r < a.rt0) {
+        n = a.ntst;
+        return a.tst + ((int64_t)b * (a.k + 1) + r) * a.ldtst;
+    }
+    n = a.nslice;
+    return a.stats + ((int64_t)b * a.Rs + (r - (int)a.rt0)) * a.nslice;
+}
 
 using Raw = uint4[kVecs];
 
@@ -192,10 +208,11 @@ __global__ __launch_bounds__(256) void greedy_final_kernel(AcceptArgs a) {
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     // wave wv merges positions wv, wv+4, ...; lanes stride over the slices
     for (int pos = wv; pos <= a.k; pos += 4) {
-        const float2* st = a.stats + ((int64_t)b * (a.k + 1) + pos) * a.nslice;
+        uint32_t nst;
+        const float2* st = row_stats(a, b, pos, nst);
         float bv = -INFINITY;
         int bi = 0x7fffffff;
-        for (int64_t c = lane; c < a.nslice; c += 64) {
+        for (int64_t c = lane; c < nst; c += 64) {
             const float2 p = st[c];
             const int pi = __float_as_int(p.y);
             if (better(p.x, pi, bv, bi)) { bv = p.x; bi = pi; }
@@ -249,15 +266,15 @@ template <bool VEC>
 __global__ __launch_bounds__(kAThreads) void stoch_stats_kernel(AcceptArgs a) {
     const int lane = threadIdx.x & (kWave - 1);
     auto row_of = [&](uint32_t row) -> const uint16_t* {
-        const int64_t b = row / a.R;
-        const int r = (int)(row % a.R);
+        const int64_t b = row / a.Rs;
+        const int r = (int)(a.rt0 + row % a.Rs);
         return (r <= a.k) ? a.zt + (b * (a.k + 1) + r) * a.V : a.zd + (b * a.k + (r - a.k - 1)) * a.V;
     };
     stream_items<VEC>(a, row_of, [&](uint32_t it, const Raw& raw) {
         const uint32_t row = it / a.nslice, c = it % a.nslice;
         const uint16_t* z = row_of(row);
         const int64_t e0 = (int64_t)c * kSlice, e1 = min(e0 + kSlice, a.V);
-        if (c == 0 && (row % a.R) == 0 && lane == 0) a.ctr[row / a.R] = 0u;   // ticket of the sample kernel
+        if (c == 0 && (row % a.Rs) == 0 && lane == 0) a.ctr[row / a.Rs] = 0u;   // ticket of the sample kernel
         const float2 r = (VEC && e1 - e0 == kSlice) ? slice_stats<VEC, true>(z, raw, e0, e1, lane, a.c2)
                                                     : slice_stats<VEC, false>(z, raw, e0, e1, lane, a.c2);
         if (lane == 0) a.stats[(int64_t)row * a.nslice + c] = r;
@@ -444,17 +461,22 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
 #pragma unroll
     for (int i = 0; i < kRowsPerWave; ++i) {
         const int r = wv + i * kWavesPerBlock;
-        first[i] = (r < (int)a.R && lane < (int)a.nslice) ? a.stats[((int64_t)b * a.R + r) * a.nslice + lane]
-                                                          : make_float2(-INFINITY, 0.0f);
+        first[i] = make_float2(-INFINITY, 0.0f);
+        if (r < (int)a.R) {
+            uint32_t nst;
+            const float2* st = row_stats(a, b, r, nst);
+            if ((uint32_t)lane < nst) first[i] = st[lane];
+        }
     }
 #pragma unroll
     for (int i = 0; i < kRowsPerWave; ++i) {
         const int r = wv + i * kWavesPerBlock;
         if (r < (int)a.R) {
-            const float2* st = a.stats + ((int64_t)b * a.R + r) * a.nslice;
+            uint32_t nst;
+            const float2* st = row_stats(a, b, r, nst);
             float m = -INFINITY, z = 0.0f;
             merge_ms(m, z, first[i].x, first[i].y);
-            for (int64_t q = lane + kWave; q < a.nslice; q += kWave) {
+            for (int64_t q = lane + kWave; q < nst; q += kWave) {
                 const float2 v = st[q];
                 merge_ms(m, z, v.x, v.y);
             }
@@ -602,6 +624,13 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     }
 }
 
+// Clears the sample kernel's tickets when no statistics kernel runs (target
+// statistics given and no draft logits to stream).
+__global__ __launch_bounds__(256) void clear_tickets_kernel(unsigned int* ctr, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) ctr[i] = 0u;
+}
+
 inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 }  // namespace
@@ -624,8 +653,10 @@ AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {
 
 hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t* zd, const int32_t* x,
                          const float* u, int64_t B, int64_t k, int64_t V, float temperature,
-                         int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream) {
+                         int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream,
+                         const float2* tstats, int64_t n_tstats, int64_t ld_tstats) {
     AcceptArgs a;
+    a.tst = tstats; a.ntst = (uint32_t)n_tstats; a.ldtst = ld_tstats;
     char* ws = reinterpret_cast<char*>(workspace);
     a.zt = zt; a.zd = zd; a.x = x; a.u = u; a.out = out_tokens; a.num = num_accepted;
     a.stats = reinterpret_cast<float2*>(ws + p.stats_off);
@@ -634,24 +665,34 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
     a.ctr = reinterpret_cast<unsigned int*>(ws + p.ctr_off);
     a.V = V; a.nchunk = p.nchunk; a.nslice = (uint32_t)p.nschunk; a.B = (int)B; a.k = (int)k;
     const bool vec = (V % 8 == 0) && ((uintptr_t)zt % 16 == 0) && (zd == nullptr || (uintptr_t)zd % 16 == 0);
+    a.rt0 = tstats ? (uint32_t)(k + 1) : 0u;
     if (temperature == 0.0f) {
         a.R = (uint32_t)(k + 1);
+        a.Rs = a.R - a.rt0;
         a.c2 = 0.0f;
-        a.items = (uint32_t)(B * a.R * p.nschunk);
-        const unsigned g1 = (unsigned)((stream_waves(a.items) + kWavesPerBlock - 1) / kWavesPerBlock);
-        if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
-        else hipLaunchKernelGGL(greedy_partial_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        a.items = (uint32_t)(B * a.Rs * p.nschunk);
+        if (a.items > 0) {
+            const unsigned g1 = (unsigned)((stream_waves(a.items) + kWavesPerBlock - 1) / kWavesPerBlock);
+            if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
+            else hipLaunchKernelGGL(greedy_partial_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
         hipLaunchKernelGGL(greedy_final_kernel, dim3((unsigned)B), dim3(256), 0, stream, a);
         return hipGetLastError();
     }
     a.R = (uint32_t)((k + 1) + (zd ? k : 0));
+    a.Rs = a.R - a.rt0;
     a.c2 = (float)(1.4426950408889634 / (double)temperature);
-    a.items = (uint32_t)(B * a.R * p.nschunk);
-    const unsigned g1 = (unsigned)((stream_waves(a.items) + kWavesPerBlock - 1) / kWavesPerBlock);
-    if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
-    else hipLaunchKernelGGL(stoch_stats_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
+    a.items = (uint32_t)(B * a.Rs * p.nschunk);
+    if (a.items > 0) {
+        const unsigned g1 = (unsigned)((stream_waves(a.items) + kWavesPerBlock - 1) / kWavesPerBlock);
+        if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
+        else hipLaunchKernelGGL(stoch_stats_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
+    } else {
+        hipLaunchKernelGGL(clear_tickets_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, stream, a.ctr,
+                           (int)B);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g2((unsigned)p.nchunk, (unsigned)B);

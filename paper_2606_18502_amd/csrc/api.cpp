@@ -62,6 +62,29 @@ spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, s
                                          workspace, as_stream(stream)));
 }
 
+size_t spec_logit_stats_count(int64_t M, int64_t V, int64_t K) {
+    if (M <= 0 || V <= 0 || K <= 0 || K % 128 != 0) return 0;
+    if (M > 2147483647LL || V > 2147483647LL || K > 2147483647LL) return 0;
+    return (size_t)specfp8::plan_gemm(M, V, K, true).stat_groups;
+}
+
+spec_status spec_fp8_gemm_logit_stats(const uint8_t* a, int64_t lda, const float* a_scale, spec_scale_mode a_mode,
+                                      const uint8_t* w, int64_t ldw, const float* w_scale, spec_scale_mode w_mode,
+                                      int64_t M, int64_t V, int64_t K, float temperature, void* logits,
+                                      int64_t ld_logits, float* stats, int64_t ld_stats, void* stream) {
+    spec_status st = specfp8::check_gemm(a, lda, a_scale, (int)a_mode, w, ldw, w_scale, (int)w_mode, M, V, K, logits,
+                                         ld_logits, SPEC_OUT_BF16);
+    if (st != SPEC_OK) return st;
+    const specfp8::GemmPlan plan = specfp8::plan_gemm(M > 0 ? M : 1, V, K, true);
+    st = specfp8::check_logit_stats(M, V, temperature, logits, ld_logits, stats, ld_stats, plan.stat_groups);
+    if (st != SPEC_OK || M == 0) return st;
+    const float c2 = temperature > 0.0f ? (float)(1.4426950408889634 / (double)temperature) : 0.0f;
+    return from_hip(specfp8::launch_gemm(plan, a, lda, a_scale, a_mode == SPEC_SCALE_PER_TENSOR, w, ldw, w_scale,
+                                         w_mode == SPEC_SCALE_PER_TENSOR, M, V, K, logits, ld_logits, 0, nullptr,
+                                         as_stream(stream), temperature > 0.0f ? 1 : 2, c2,
+                                         reinterpret_cast<float2*>(stats), ld_stats));
+}
+
 size_t spec_verify_accept_workspace_bytes(int64_t B, int64_t k, int64_t V) {
     if (B <= 0 || k < 1 || V < 1) return 0;
     return specfp8::plan_accept(B, k, V).bytes;
@@ -83,6 +106,26 @@ spec_status spec_verify_accept(const void* target_logits, const void* draft_logi
                                            as_stream(stream)));
 }
 
+spec_status spec_verify_accept_stats(const void* target_logits, const float* target_stats, int64_t n_stats,
+                                     int64_t ld_stats, const void* draft_logits, const int32_t* draft_tokens,
+                                     const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
+                                     int32_t* out_tokens, int32_t* num_accepted, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+    spec_status st = specfp8::check_accept(target_logits, draft_logits, draft_tokens, uniforms, B, k, V, temperature,
+                                           out_tokens, num_accepted);
+    if (st != SPEC_OK) return st;
+    st = specfp8::check_accept_stats(target_stats, n_stats, ld_stats, B);
+    if (st != SPEC_OK || B == 0) return st;
+    const specfp8::AcceptPlan plan = specfp8::plan_accept(B, k, V);
+    if (!workspace || workspace_bytes < plan.bytes) return SPEC_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return SPEC_ERR_ALIGN;
+    return from_hip(specfp8::launch_accept(plan, reinterpret_cast<const uint16_t*>(target_logits),
+                                           reinterpret_cast<const uint16_t*>(draft_logits), draft_tokens, uniforms,
+                                           B, k, V, temperature, out_tokens, num_accepted, workspace,
+                                           as_stream(stream), reinterpret_cast<const float2*>(target_stats),
+                                           n_stats, ld_stats));
+}
+
 const char* spec_status_string(spec_status s) {
     switch (s) {
         case SPEC_OK: return "ok";
@@ -100,6 +143,6 @@ const char* spec_status_string(spec_status s) {
 
 int spec_last_hip_error(void) { return g_last_hip_error; }
 
-int spec_version(void) { return 100; }
+int spec_version(void) { return 200; }
 
 }  // extern "C"

@@ -54,10 +54,13 @@ struct GemmArgs {
     const float* sw;
     void* y;
     float* partial;   // [splits][M][ldp] when splits > 1
-    int64_t lda, ldw, ldy, ldp;
+    float2* stats;    // [M][ld_stats] column-group statistics of the bf16 output (stats_mode != 0)
+    int64_t lda, ldw, ldy, ldp, ld_stats;
     int M, N, K;
     int a_per_tensor, w_per_tensor, out_f32;
     int m_tiles, n_tiles, splits, ksteps;
+    int stats_mode;   // 0: none; 1: (max t, sum 2^(t - max)), t = z * c2; 2: (max z, lowest column)
+    float c2;
 };
 
 __device__ __forceinline__ int xcd_remap(int b, int total) {
@@ -325,7 +328,80 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[W
     }
 }
 
-template <int WTM, int WTN, int WM, int WN, int STAGES>
+__device__ __forceinline__ bool beats(float v, int i, float bv, int bi) {
+    return v > bv || (v == bv && i < bi);
+}
+
+// Statistics of the stored (bf16-rounded) outputs, per row, over the columns
+// one wave holds (column group nt * WN + wn of the row): the acceptance
+// statistics of a logit row computed where the logits are produced.
+//   mode 1: (M, Z) with t = fl32(z * c2): M = fl32(max z * c2) (c2 > 0), then
+//           Z = sum 2^fma(z, c2, -M) with one exponential per element and no
+//           rescaling; an all-empty group stores (-inf, 0).
+//   mode 2: (max z, lowest column holding it, as int bits); empty: (-inf, INT_MAX).
+// Each row's values sit in the 4 lanes r16 + 16 kg of the wave; they are
+// combined with two xor shuffles in a fixed order.  The scales and rounding
+// are those of store_tile, so the statistics describe exactly the stored Y.
+template <int WTM, int WTN, int WN>
+__device__ __forceinline__ void tile_stats(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
+                                           const float (&sw_reg)[WTN][4], int m0, int n0, int wm, int wn, int nt,
+                                           int lane) {
+    const int kg = lane >> 4;
+    const int r16 = lane & 15;
+    const int64_t col = (int64_t)nt * WN + wn;
+    // the stored value of output (i, r) of row block j, or -inf past the last column
+    auto zval = [&](int i, int j, int r) {
+        const int n = n0 + (wn * WTN + i) * 16 + 4 * kg + r;
+        const float y = (acc[i][j][r] * sa_reg[j]) * sw_reg[i][r];
+        return n < g.N ? bf16_to_f32(f32_to_bf16_rne(y)) : -INFINITY;
+    };
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) {
+        const int m = m0 + (wm * WTM + j) * 16 + r16;
+        float2 out;
+        if (g.stats_mode == 2) {
+            float bv = -INFINITY;
+            int bi = 0x7fffffff;
+#pragma unroll
+            for (int i = 0; i < WTN; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int n = n0 + (wn * WTN + i) * 16 + 4 * kg + r;
+                    const float v = zval(i, j, r);
+                    if (n < g.N && beats(v, n, bv, bi)) { bv = v; bi = n; }
+                }
+#pragma unroll
+            for (int o = 16; o <= 32; o <<= 1) {
+                const float ov = __shfl_xor(bv, o, 64);
+                const int oi = __shfl_xor(bi, o, 64);
+                if (beats(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+            }
+            out = make_float2(bv, __int_as_float(bi));
+        } else {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < WTN; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, zval(i, j, r));
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const float M = mx * g.c2;
+            float s = 0.0f;
+            if (M != -INFINITY) {
+#pragma unroll
+                for (int i = 0; i < WTN; ++i)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) s += __builtin_amdgcn_exp2f(fmaf(zval(i, j, r), g.c2, -M));
+            }
+            s += __shfl_xor(s, 16, 64);
+            s += __shfl_xor(s, 32, 64);
+            out = make_float2(M, s);
+        }
+        if (kg == 0 && m < g.M) g.stats[(int64_t)m * g.ld_stats + col] = out;
+    }
+}
+
+template <int WTM, int WTN, int WM, int WN, int STAGES, bool STATS>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     using C = GemmCfg<WTM, WTN, WM, WN, STAGES>;
     static_assert(STAGES >= 2 && STAGES <= 4, "2..4 stages");
@@ -411,6 +487,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     wait_vmcnt<0>();   // no direct-to-LDS write may outlive the workgroup
 
     store_tile<WTM, WTN>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split);
+    if constexpr (STATS) tile_stats<WTM, WTN, WN>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, nt, lane);
 }
 
 // Sum the split-K partials in split order, then scale and convert.
@@ -477,29 +554,46 @@ constexpr int kKinds = 9;
 
 constexpr int kCfgBM[kKinds] = {Cfg0::BM, Cfg1::BM, Cfg2::BM, Cfg3::BM, Cfg4::BM, Cfg5::BM, Cfg6::BM, Cfg7::BM, Cfg8::BM};
 constexpr int kCfgBN[kKinds] = {Cfg0::BN, Cfg1::BN, Cfg2::BN, Cfg3::BN, Cfg4::BN, Cfg5::BN, Cfg6::BN, Cfg7::BN, Cfg8::BN};
+constexpr int kCfgWN[kKinds] = {2, 2, 2, 2, 2, 2, 1, 2, 2};   // waves across N (statistics groups per tile)
 
+// The statistics epilogue is a separate instantiation, so the plain GEMMs'
+// register allocation does not carry it.
 template <class C, int WTM, int WTN, int WM, int WN, int STAGES>
 hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
     const int total = g.m_tiles * g.n_tiles * g.splits;
-    hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES>), dim3(total), dim3(C::kThreads), 0, stream, g);
+    if (g.stats_mode != 0)
+        hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, true>), dim3(total), dim3(C::kThreads), 0,
+                           stream, g);
+    else
+        hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, false>), dim3(total), dim3(C::kThreads), 0,
+                           stream, g);
     return hipGetLastError();
 }
 
 }  // namespace
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool no_split) {
     GemmPlan p{};
     // Tile shapes by measurement on MI355X (M = B*(k+1) verify rows):
     //   M <= 64: 64x64;  M <= 80: 80x128;
     //   M <= 320: 160x224 when N fills >= 64 such columns exactly (gate|up),
+    //             else for very wide N (an LM head) 160x192 (or 160x224
+    //             with a ragged last tile),
     //             160x128 with a K split for long-K layers (down), else
     //             64x128 (QKV, O: a CU's time is set by the operand rows it
     //             streams per K-step, 192 here against 224 for 160x64);
     //   larger M: 160x224.
     if (M <= 64) p.kind = 0;
     else if (M <= 80) p.kind = 1;
-    else if (M <= 320) p.kind = (N % 224 == 0 && N >= 224 * 64) ? 2 : (K >= 2 * N ? 5 : 8);
+    else if (M <= 320) {
+        if (N % 224 == 0 && N >= 224 * 64) p.kind = 2;
+        else if (N >= 192 * 64) p.kind = (N % 192 == 0) ? 4 : 2;
+        else p.kind = K >= 2 * N ? 5 : 8;
+    }
     else p.kind = 2;
+    // with the statistics epilogue the 160x224 tile would spill registers;
+    // 160x192 (ragged last tile where N % 192 != 0) takes its place
+    if (no_split && p.kind == 2) p.kind = 4;
     const int ksteps = (int)(K / kBK);
     int splits = 0;
 #ifdef SPECFP8_TUNING
@@ -513,6 +607,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
     p.m_tiles = (int)((M + bm - 1) / bm);
     p.n_tiles = (int)((N + bn - 1) / bn);
     const int tiles = p.m_tiles * p.n_tiles;
+    if (no_split) splits = 1;
     if (splits <= 0) {
         // Split K only when at most half of the 256 compute units would get
         // a tile, and keep the split grid under ~200 workgroups: every split
@@ -528,6 +623,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
     // every split must own at least one K-step after ceil division
     while (splits > 1 && (int64_t)((ksteps + splits - 1) / splits) * (splits - 1) >= ksteps) --splits;
     p.splits = splits;
+    p.stat_groups = (int64_t)p.n_tiles * kCfgWN[p.kind];
     p.ldp = (N + 3) / 4 * 4;
     p.workspace_bytes = splits > 1 ? (size_t)splits * (size_t)M * (size_t)p.ldp * sizeof(float) : 0;
     return p;
@@ -536,8 +632,9 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K) {
 hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const float* sa, int a_per_tensor,
                        const uint8_t* w, int64_t ldw, const float* sw, int w_per_tensor, int64_t M,
                        int64_t N, int64_t K, void* y, int64_t ldy, int out_f32, void* workspace,
-                       hipStream_t stream) {
+                       hipStream_t stream, int stats_mode, float c2, float2* stats, int64_t ld_stats) {
     GemmArgs g;
+    g.stats = stats; g.ld_stats = ld_stats; g.stats_mode = stats_mode; g.c2 = c2;
     g.a = a; g.w = w; g.sa = sa; g.sw = sw; g.y = y;
     g.partial = reinterpret_cast<float*>(workspace);
     g.lda = lda; g.ldw = ldw; g.ldy = ldy; g.ldp = p.ldp;

@@ -18,14 +18,20 @@ struct GemmPlan {
     int kind;              // tile configuration
     int m_tiles, n_tiles;  // output tiles
     int splits;            // K-splits (1 = none)
+    int64_t stat_groups;   // column groups per row of the epilogue statistics (n_tiles * waves across N)
     int64_t ldp;           // row stride of the fp32 partial tiles
     size_t workspace_bytes;
 };
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K);
+// no_split: one workgroup per output tile (required for epilogue statistics)
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool no_split = false);
+// stats_mode 0: plain GEMM; 1/2: also the per-(row, column group) statistics
+// of the bf16 output (softmax in base 2 with c2 = log2(e)/T, or argmax) into
+// stats [M][ld_stats]; requires p.splits == 1.
 hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const float* sa, int a_per_tensor,
                        const uint8_t* w, int64_t ldw, const float* sw, int w_per_tensor, int64_t M,
                        int64_t N, int64_t K, void* y, int64_t ldy, int out_f32, void* workspace,
-                       hipStream_t stream);
+                       hipStream_t stream, int stats_mode = 0, float c2 = 0.0f, float2* stats = nullptr,
+                       int64_t ld_stats = 0);
 
 // ---- accept.hip
 struct AcceptPlan {
@@ -36,8 +42,11 @@ struct AcceptPlan {
     size_t stats_off, mass_off, fine_off, ctr_off, bytes;
 };
 AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V);
+// tstats (optional): the target rows' statistics [B*(k+1)][ld_tstats], n_tstats
+// entries per row, in the form the GEMM epilogue writes for this temperature.
 hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t* zd, const int32_t* x,
                          const float* u, int64_t B, int64_t k, int64_t V, float temperature,
-                         int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream);
+                         int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream,
+                         const float2* tstats = nullptr, int64_t n_tstats = 0, int64_t ld_tstats = 0);
 
 }  // namespace specfp8

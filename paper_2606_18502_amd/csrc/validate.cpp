@@ -63,6 +63,28 @@ spec_status check_gemm(const void* a, int64_t lda, const float* a_scale, int a_m
     return SPEC_OK;
 }
 
+// The LM-head variant's own arguments (the GEMM operands are checked by
+// check_gemm with N = V, y = logits, bf16 out).
+spec_status check_logit_stats(int64_t M, int64_t V, float temperature, const void* logits, int64_t ld_logits,
+                              const float* stats, int64_t ld_stats, int64_t n_groups) {
+    (void)V; (void)logits; (void)ld_logits;
+    if (!isfinite(temperature) || temperature < 0.0f) return SPEC_ERR_VALUE;
+    if (ld_stats < n_groups) return SPEC_ERR_SHAPE;
+    if (M == 0) return SPEC_OK;
+    if (!stats) return SPEC_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(stats) & 7u) return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
+spec_status check_accept_stats(const float* target_stats, int64_t n_stats, int64_t ld_stats, int64_t B) {
+    if (n_stats < 1 || ld_stats < n_stats) return SPEC_ERR_SHAPE;
+    if (n_stats > 2147483647LL) return SPEC_ERR_UNSUPPORTED;
+    if (B == 0) return SPEC_OK;
+    if (!target_stats) return SPEC_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(target_stats) & 7u) return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
 spec_status check_accept(const void* target_logits, const void* draft_logits, const int32_t* draft_tokens,
                          const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
                          const int32_t* out_tokens, const int32_t* num_accepted) {

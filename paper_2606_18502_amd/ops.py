@@ -147,6 +147,58 @@ def gemm(a: torch.Tensor, sa: torch.Tensor, w: torch.Tensor, sw: torch.Tensor,
     return out
 
 
+def _scale_modes(a, sa, w, sw):
+    M, N = a.shape[0], w.shape[0]
+    a_mode = _lib.SCALE_PER_TENSOR if sa.numel() == 1 and M != 1 else _lib.SCALE_PER_ROW
+    w_mode = _lib.SCALE_PER_TENSOR if sw.numel() == 1 and N != 1 else _lib.SCALE_PER_ROW
+    if a_mode == _lib.SCALE_PER_ROW and sa.numel() < M:
+        raise ValueError("sa must hold M per-row scales or one per-tensor scale")
+    if w_mode == _lib.SCALE_PER_ROW and sw.numel() < N:
+        raise ValueError("sw must hold N per-channel scales or one per-tensor scale")
+    return a_mode, w_mode
+
+
+def logit_stats_count(M: int, V: int, K: int) -> int:
+    return int(_lib.load().spec_logit_stats_count(M, V, K))
+
+
+def gemm_logit_stats(a: torch.Tensor, sa: torch.Tensor, w: torch.Tensor, sw: torch.Tensor, temperature: float,
+                     out: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None
+                     ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """LM-head GEMM with the acceptance statistics in its epilogue (spec_fp8_gemm_logit_stats).
+
+    a: uint8 E4M3 [M,K] (final hidden states of the verify rows); w: uint8 E4M3 [V,K];
+    sa, sw as for gemm.  Returns (logits bf16 [M,V], stats fp32 [M,G,2]) with
+    G = logit_stats_count(M, V, K) column groups per row.
+    """
+    lib = _lib.load()
+    _dev(a, torch.uint8, "a")
+    _dev(w, torch.uint8, "w")
+    _dev(sa, torch.float32, "sa")
+    _dev(sw, torch.float32, "sw")
+    M, K = a.shape
+    V = w.shape[0]
+    if w.shape[1] != K:
+        raise ValueError("a and w disagree on K")
+    a_mode, w_mode = _scale_modes(a, sa, w, sw)
+    G = logit_stats_count(M, V, K)
+    if out is None:
+        ld = (V + 7) // 8 * 8
+        out = torch.empty((M, ld), dtype=torch.bfloat16, device=a.device)[:, :V]
+    _dev(out, torch.bfloat16, "out")
+    if stats is None:
+        stats = torch.empty((M, G, 2), dtype=torch.float32, device=a.device)
+    _dev(stats, torch.float32, "stats")
+    if stats.dim() != 3 or stats.shape[0] != M or stats.shape[2] != 2 or stats.stride(2) != 1 or \
+            stats.stride(1) != 2:
+        raise ValueError("stats must be [M, >=G, 2] with contiguous pairs")
+    check("spec_fp8_gemm_logit_stats", lib.spec_fp8_gemm_logit_stats(
+        a.data_ptr(), _rowmajor(a, "a"), sa.data_ptr(), a_mode, w.data_ptr(), _rowmajor(w, "w"), sw.data_ptr(),
+        w_mode, M, V, K, float(temperature), out.data_ptr(), _rowmajor(out, "out"), stats.data_ptr(),
+        stats.stride(0) // 2, _stream()))
+    return out, stats
+
+
 def accept_workspace_bytes(B: int, k: int, V: int) -> int:
     return int(_lib.load().spec_verify_accept_workspace_bytes(B, k, V))
 
@@ -154,12 +206,14 @@ def accept_workspace_bytes(B: int, k: int, V: int) -> int:
 def verify_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor], draft_tokens: torch.Tensor,
                   uniforms: Optional[torch.Tensor], temperature: float,
                   workspace: Optional[torch.Tensor] = None,
-                  out_tokens: Optional[torch.Tensor] = None, num_accepted: Optional[torch.Tensor] = None
-                  ) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Greedy (T=0) or speculative-sampling (T>0) acceptance (spec_verify_accept).
+                  out_tokens: Optional[torch.Tensor] = None, num_accepted: Optional[torch.Tensor] = None,
+                  target_stats: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Greedy (T=0) or speculative-sampling (T>0) acceptance (spec_verify_accept, or
+    spec_verify_accept_stats when target_stats from gemm_logit_stats are given).
 
     target_logits bf16 [B,k+1,V]; draft_logits bf16 [B,k,V] or None;
-    draft_tokens int32 [B,k]; uniforms fp32 [B,k+1] (T>0).
+    draft_tokens int32 [B,k]; uniforms fp32 [B,k+1] (T>0);
+    target_stats fp32 [B*(k+1), G, 2] (pairs) or None.
     Returns (out_tokens int32 [B,k+1] (-1 padded), num_accepted int32 [B]).
     """
     lib = _lib.load()
@@ -186,9 +240,21 @@ def verify_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tens
     need = accept_workspace_bytes(B, k, V)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=target_logits.device)
-    check("spec_verify_accept", lib.spec_verify_accept(
-        target_logits.data_ptr(), None if draft_logits is None else draft_logits.data_ptr(),
-        draft_tokens.data_ptr(), None if uniforms is None else uniforms.data_ptr(), B, k, V,
-        float(temperature), out_tokens.data_ptr(), num_accepted.data_ptr(), workspace.data_ptr(),
-        workspace.numel() * workspace.element_size(), _stream()))
+    if target_stats is None:
+        check("spec_verify_accept", lib.spec_verify_accept(
+            target_logits.data_ptr(), None if draft_logits is None else draft_logits.data_ptr(),
+            draft_tokens.data_ptr(), None if uniforms is None else uniforms.data_ptr(), B, k, V,
+            float(temperature), out_tokens.data_ptr(), num_accepted.data_ptr(), workspace.data_ptr(),
+            workspace.numel() * workspace.element_size(), _stream()))
+    else:
+        _dev(target_stats, torch.float32, "target_stats")
+        if target_stats.dim() != 3 or target_stats.shape[0] != B * k1 or target_stats.shape[2] != 2 or \
+                target_stats.stride(2) != 1 or target_stats.stride(1) != 2:
+            raise ValueError("target_stats must be [B*(k+1), G, 2] with contiguous pairs")
+        check("spec_verify_accept_stats", lib.spec_verify_accept_stats(
+            target_logits.data_ptr(), target_stats.data_ptr(), target_stats.shape[1], target_stats.stride(0) // 2,
+            None if draft_logits is None else draft_logits.data_ptr(), draft_tokens.data_ptr(),
+            None if uniforms is None else uniforms.data_ptr(), B, k, V, float(temperature), out_tokens.data_ptr(),
+            num_accepted.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+            _stream()))
     return out_tokens, num_accepted

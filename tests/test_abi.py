@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.spec_version() == 100
+    assert lib.spec_version() == 200
     for s in range(9):
         assert lib.spec_status_string(s)
     assert lib.spec_status_string(99) == b"unknown status"
@@ -151,3 +151,53 @@ def test_workspace_sizes_grow_with_problem(lib):
     assert lib.spec_verify_accept_workspace_bytes(64, 4, 128256) > lib.spec_verify_accept_workspace_bytes(2, 3, 256)
     assert lib.spec_verify_accept_workspace_bytes(0, 3, 256) == 0
     assert lib.spec_fp8_gemm_workspace_bytes(4096, 14336, 4096) == 0     # enough tiles: no split
+
+
+def ls(lib, a=A16, lda=512, sa=A16, am=0, w=A16, ldw=512, sw=A16, wm=0, M=8, V=1024, K=512, T=0.7,
+       y=A16, ldy=1024, st=A16, ldst=None):
+    if ldst is None:
+        ldst = lib.spec_logit_stats_count(M, V, K)
+    return lib.spec_fp8_gemm_logit_stats(a, lda, sa, am, w, ldw, sw, wm, M, V, K, ctypes.c_float(T), y, ldy, st,
+                                         ldst, None)
+
+
+def test_logit_stats_gemm_validation(lib):
+    G = lib.spec_logit_stats_count(8, 1024, 512)
+    assert G >= 1
+    assert lib.spec_logit_stats_count(320, 128256, 4096) >= 128256 // 224      # one group per wave column
+    assert lib.spec_logit_stats_count(8, 1024, 100) == 0                         # K % 128
+    assert lib.spec_logit_stats_count(0, 1024, 512) == 0
+    # the GEMM operand checks come first and are those of spec_fp8_gemm
+    assert ls(lib, am=2) == ENUM
+    assert ls(lib, K=500, lda=512, ldw=512) == UNSUP
+    assert ls(lib, ldy=512) == SHAPE
+    assert ls(lib, a=None) == NULL
+    assert ls(lib, ldy=1028) == ALIGN
+    # then the statistics' own
+    assert ls(lib, T=float("nan")) == VALUE
+    assert ls(lib, T=-1.0) == VALUE
+    assert ls(lib, ldst=G - 1) == SHAPE
+    assert ls(lib, st=None) == NULL
+    assert ls(lib, st=A16 + 4) == ALIGN
+    assert ls(lib, M=0, a=None, sa=None, w=None, sw=None, y=None, st=None, ldst=G) == OK
+
+
+def accs(lib, zt=A16, ts=A16, n=4, ldn=4, zd=A16, x=A16, u=A16, B=2, k=3, V=256, T=0.7, out=A16, num=A16, ws=A16,
+         wsb=1 << 20):
+    return lib.spec_verify_accept_stats(zt, ts, n, ldn, zd, x, u, B, k, V, ctypes.c_float(T), out, num, ws, wsb, None)
+
+
+def test_accept_stats_validation(lib):
+    # the checks of spec_verify_accept come first
+    assert accs(lib, T=-0.5) == VALUE
+    assert accs(lib, k=0) == SHAPE
+    assert accs(lib, zt=None) == NULL
+    # then the target statistics
+    assert accs(lib, n=0) == SHAPE
+    assert accs(lib, n=5, ldn=4) == SHAPE
+    assert accs(lib, n=1 << 31, ldn=1 << 31) == UNSUP
+    assert accs(lib, ts=None) == NULL
+    assert accs(lib, ts=A16 + 4) == ALIGN
+    assert accs(lib, ws=None) == WS
+    assert accs(lib, B=0, zt=None, ts=None, zd=None, x=None, u=None, out=None, num=None, ws=None, wsb=0) == OK
+    assert accs(lib, T=0.0, u=None, zd=None, ws=None) == WS             # greedy: no uniforms, no draft logits

@@ -183,3 +183,34 @@ def test_margins_reported():
     assert mg.shape == (3,) and np.all(mg >= 0)
     out2, num2 = oa.accept_stochastic(zt, zd, x, u, 0.7)
     np.testing.assert_array_equal(out, out2)
+
+
+# ---- softmax normalizer (the statistics an LM-head epilogue hands to the acceptance)
+
+def test_softmax_normalizer_constant_row_is_vocabulary_size():
+    for V in (1, 7, 4096, 128256):
+        zmax, Z = oa.softmax_normalizer(_bits(np.full(V, -3.25)), 0.7)
+        assert zmax == -3.25 and Z == V
+
+
+def test_softmax_normalizer_two_level_closed_form():
+    # one logit a, V-1 logits b: Z = 1 + (V-1) e^((b-a)/T)
+    V, a, b, T = 1000, 2.0, 0.5, 0.5
+    z = np.full(V, b)
+    z[417] = a
+    zmax, Z = oa.softmax_normalizer(_bits(z), T)
+    assert zmax == a
+    assert abs(Z - (1 + (V - 1) * np.exp((b - a) / T))) <= 1e-12 * Z
+
+
+def test_softmax_normalizer_shift_and_batch():
+    rng = np.random.default_rng(3)
+    z = np.round(rng.normal(0, 4, size=(3, 5, 300)))            # integers: shifts by 8 stay exact in bf16
+    zmax, Z = oa.softmax_normalizer(_bits(z), 1.3)
+    zmax2, Z2 = oa.softmax_normalizer(_bits(z + 8), 1.3)
+    assert zmax.shape == Z.shape == (3, 5)
+    np.testing.assert_array_equal(zmax2, zmax + 8)
+    np.testing.assert_allclose(Z2, Z, rtol=1e-14)
+    # a very high temperature flattens the distribution towards uniform
+    _, Zhot = oa.softmax_normalizer(_bits(z), 1e7)
+    np.testing.assert_allclose(Zhot, 300, rtol=1e-5)
