@@ -169,6 +169,61 @@ def vendor_gemm(torch, step, weights, reps=22):
     return res
 
 
+def lm_head_parts(torch, p, wl, reps=12):
+    """The LM head of the verify pass (M = 320 rows, K = 4096 -> V = 128256)
+    followed by the stochastic acceptance, two ways: unfused (the GEMM writes
+    the logits, the acceptance reads them for its statistics) and fused (the
+    statistics come out of the GEMM epilogue and the acceptance streams only
+    the draft rows).  Seeded synthetic weights and hidden states made on the
+    device; each part timed like time_parts.  Returns mean us per part."""
+    cfg4 = wl.CONFIGS["C4"]
+    B, k, V, T = cfg4["B"], cfg4["k"], cfg4["V"], cfg4["temperature"]
+    K, M = 4096, B * (cfg4["k"] + 1)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(20260)
+    w_bf = (torch.randn((V, K), generator=g, device="cuda") * 0.05).to(torch.bfloat16)
+    w, sw = p.quantize(w_bf)
+    del w_bf
+    xt = torch.randn((M, K), generator=g, device="cuda")
+    xd = (xt.view(B, k + 1, K)[:, :k] + 0.5 * torch.randn((B, k, K), generator=g, device="cuda")).reshape(B * k, K)
+    a_t, sa_t = p.quantize(xt.to(torch.bfloat16))
+    a_d, sa_d = p.quantize(xd.to(torch.bfloat16))
+    zd = p.gemm(a_d, sa_d, w, sw).view(B, k, V)
+    probs = torch.softmax(zd.float().view(B * k, V) / T, dim=-1)
+    x = torch.multinomial(probs, 1, generator=g).view(B, k).to(torch.int32)
+    del probs
+    u = torch.rand((B, k + 1), generator=g, device="cuda")
+    logits = torch.empty((M, V), dtype=torch.bfloat16, device="cuda")
+    stats = torch.empty((M, p.logit_stats_count(M, V, K), 2), dtype=torch.float32, device="cuda")
+    ws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device="cuda")
+    out = torch.empty((B, k + 1), dtype=torch.int32, device="cuda")
+    num = torch.empty((B,), dtype=torch.int32, device="cuda")
+    zt = logits.view(B, k + 1, V)
+    parts = {
+        "gemm": lambda: p.gemm(a_t, sa_t, w, sw, out=logits),
+        "gemm_with_stats": lambda: p.gemm_logit_stats(a_t, sa_t, w, sw, T, out=logits, stats=stats),
+        "accept": lambda: p.verify_accept(zt, zd, x, u, T, workspace=ws, out_tokens=out, num_accepted=num),
+        "accept_from_stats": lambda: p.verify_accept(zt, zd, x, u, T, workspace=ws, out_tokens=out,
+                                                     num_accepted=num, target_stats=stats),
+    }
+    res = {}
+    for n, fn in parts.items():
+        evs = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        res[n] = round(float(np.mean([a.elapsed_time(b) for a, b in evs[2:]])) * 1e3, 1)
+    res["unfused_us"] = round(res["gemm"] + res["accept"], 1)
+    res["fused_us"] = round(res["gemm_with_stats"] + res["accept_from_stats"], 1)
+    res["gemm_tflops"] = round(2.0 * M * V * K / (res["gemm"] * 1e-6) / 1e12, 1)
+    res["workload"] = f"LM head M={M} K={K} V={V} (bf16 logits) + stochastic acceptance T={T}, k={k}"
+    return res
+
+
 def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40):
     """The oracle on the host cores, on a bounded sample of the benched step:
     the 4 linears at M=320 restricted to every `nfrac`-th output channel
@@ -339,6 +394,9 @@ def main(argv=None):
 
     parts, spread = time_parts(torch, step, weights, logits, reps=22)
     vendor = vendor_gemm(torch, step, weights)
+    lm = lm_head_parts(torch, p, wl)
+    log(f"LM head: gemm {lm['gemm']} us (with statistics {lm['gemm_with_stats']}); accept {lm['accept']} us "
+        f"(from statistics {lm['accept_from_stats']}); unfused {lm['unfused_us']} us, fused {lm['fused_us']} us")
     gemm_us = parts["qkv"] + parts["o"] + parts["gate_up"] + parts["down"]
     gu_us, acc_us = parts["gate_up"], parts["accept"]
     log(f"step {ms_step * 1e3:.1f} us (eager), {ms_step_graph * 1e3:.1f} us (graph); gate_up gemm {gu_us:.1f} us; "
@@ -369,6 +427,7 @@ def main(argv=None):
             "gemm_us": {n: round(parts[n], 1) for n in ("qkv", "o", "gate_up", "down")},
             "hipblaslt_gemm_us": vendor,
             "part_us_p10_p90": spread,
+            "lm_head_and_accept_us": lm,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),

@@ -158,9 +158,11 @@ spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, s
  *   for every row m and column group c, 0 <= c < spec_logit_stats_count(M, V, K)
  *   (a group is a contiguous range of columns; the groups, in column order,
  *   partition [0, V); a group may be empty):
- *     temperature > 0:  c2 = fl32(log2(e) / T),
- *                       Mc = fl32(max_{n in c} z[m,n] * c2),
- *                       Zc = sum_{n in c} 2^fl32(fma(z[m,n], c2, -Mc))   (fp32, order unspecified)
+ *     temperature > 0:  c2 = fl32(log2(e) / T), t_n = fl32(z[m,n] * c2),
+ *                       Mc = max_{n in c} t_n  (= fl32(max z * c2)),
+ *                       Zc = sum_{n in c} 2^(t_n - Mc), evaluated in fp32 in an
+ *                            unspecified order (partial sums are rescaled as the
+ *                            running maximum grows)
  *                       stats[m,c] = (Mc, Zc); an empty group is (-inf, 0)
  *     temperature == 0: stats[m,c] = (max_{n in c} z[m,n], lowest n attaining it as int32 bits);
  *                       an empty group is (-inf, INT32_MAX as int32 bits)

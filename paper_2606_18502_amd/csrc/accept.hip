@@ -212,10 +212,20 @@ __global__ __launch_bounds__(256) void greedy_final_kernel(AcceptArgs a) {
         const float2* st = row_stats(a, b, pos, nst);
         float bv = -INFINITY;
         int bi = 0x7fffffff;
-        for (int64_t c = lane; c < nst; c += 64) {
-            const float2 p = st[c];
-            const int pi = __float_as_int(p.y);
-            if (better(p.x, pi, bv, bi)) { bv = p.x; bi = pi; }
+        // loads issued 8 per lane before they are compared (a row may hold
+        // over a thousand entries when they come from the LM-head epilogue)
+        for (int64_t c0 = lane; c0 < nst; c0 += 8 * 64) {
+            float2 pv[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int64_t c = c0 + q * 64;
+                pv[q] = c < nst ? st[c] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int pi = __float_as_int(pv[q].y);
+                if (better(pv[q].x, pi, bv, bi)) { bv = pv[q].x; bi = pi; }
+            }
         }
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) {
@@ -476,9 +486,16 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
             const float2* st = row_stats(a, b, r, nst);
             float m = -INFINITY, z = 0.0f;
             merge_ms(m, z, first[i].x, first[i].y);
-            for (int64_t q = lane + kWave; q < nst; q += kWave) {
-                const float2 v = st[q];
-                merge_ms(m, z, v.x, v.y);
+            // loads issued 8 per lane before they are merged, in entry order
+            for (int64_t q0 = lane + kWave; q0 < nst; q0 += 8 * kWave) {
+                float2 v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int64_t q = q0 + u * kWave;
+                    v[u] = q < nst ? st[q] : make_float2(-INFINITY, 0.0f);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) merge_ms(m, z, v[u].x, v[u].y);
             }
             const float M = wave_max(m);
             const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));

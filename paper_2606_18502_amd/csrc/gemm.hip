@@ -27,6 +27,8 @@
 // Workgroup ids are remapped so that the tiles and K-splits that share
 // operands run on the same XCD (blocks are dealt round-robin to the 8 XCDs),
 // which keeps re-read operand bytes in that XCD's L2.
+#include <float.h>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -278,130 +280,167 @@ __device__ __forceinline__ void load_scales(const GemmArgs& g, float (&sa_reg)[W
         }
 }
 
-// Epilogue: lane holds D[n = 4*(lane/16) + r][m = lane%16] of each 16x16
-// block; the scales were fetched into registers before the main loop.  With a
-// K split the fp32 partial goes to the workspace instead.
-template <int WTM, int WTN>
-__device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
-                                           const float (&sw_reg)[WTN][4], int m0, int n0, int wm, int wn, int lane,
-                                           int split) {
-    const int kg = lane >> 4;
-    const int r16 = lane & 15;
-#pragma unroll
-    for (int i = 0; i < WTN; ++i) {
-        const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
-#pragma unroll
-        for (int j = 0; j < WTM; ++j) {
-            const int m = m0 + (wm * WTM + j) * 16 + r16;
-            const v4f a = acc[i][j];
-            const bool ok = (n < g.N) && (m < g.M);
-            if (g.splits > 1) {
-                if (ok) {
-                    float* dst = g.partial + ((int64_t)split * g.M + m) * g.ldp + n;
-                    *reinterpret_cast<float4*>(dst) = make_float4(a[0], a[1], a[2], a[3]);
-                }
-                continue;
-            }
-            float y[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) y[r] = (a[r] * sa_reg[j]) * sw_reg[i][r];
-            if (!ok) continue;
-            if (g.out_f32) {
-                float* dst = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-                if (n + 3 < g.N) {
-                    *reinterpret_cast<float4*>(dst) = make_float4(y[0], y[1], y[2], y[3]);
-                } else {
-                    for (int r = 0; r < 4 && n + r < g.N; ++r) dst[r] = y[r];
-                }
-            } else {
-                uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-                if (n + 3 < g.N) {
-                    uint2 o;
-                    o.x = f32_to_bf16_rne(y[0]) | (f32_to_bf16_rne(y[1]) << 16);
-                    o.y = f32_to_bf16_rne(y[2]) | (f32_to_bf16_rne(y[3]) << 16);
-                    *reinterpret_cast<uint2*>(dst) = o;
-                } else {
-                    for (int r = 0; r < 4 && n + r < g.N; ++r) dst[r] = (uint16_t)f32_to_bf16_rne(y[r]);
-                }
-            }
-        }
-    }
-}
-
 __device__ __forceinline__ bool beats(float v, int i, float bv, int bi) {
     return v > bv || (v == bv && i < bi);
 }
 
-// Statistics of the stored (bf16-rounded) outputs, per row, over the columns
-// one wave holds (column group nt * WN + wn of the row): the acceptance
-// statistics of a logit row computed where the logits are produced.
-//   mode 1: (M, Z) with t = fl32(z * c2): M = fl32(max z * c2) (c2 > 0), then
-//           Z = sum 2^fma(z, c2, -M) with one exponential per element and no
-//           rescaling; an all-empty group stores (-inf, 0).
-//   mode 2: (max z, lowest column holding it, as int bits); empty: (-inf, INT_MAX).
-// Each row's values sit in the 4 lanes r16 + 16 kg of the wave; they are
-// combined with two xor shuffles in a fixed order.  The scales and rounding
-// are those of store_tile, so the statistics describe exactly the stored Y.
-template <int WTM, int WTN, int WN>
-__device__ __forceinline__ void tile_stats(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
-                                           const float (&sw_reg)[WTN][4], int m0, int n0, int wm, int wn, int nt,
-                                           int lane) {
+// Online (max, sum 2^(t - max)) of one more value t: one exponential of
+// -|t - m| per value, the running sum rescaled when the maximum moves.  The
+// running max starts at the finite sentinel -FLT_MAX, so that t = -inf (a
+// column past the edge) adds exactly 0 without a branch.
+__device__ __forceinline__ void online_add(float& m, float& s, float t) {
+    const float d = t - m;
+    const float e = __builtin_amdgcn_exp2f(-fabsf(d));
+    const bool up = d > 0.0f;
+    s = up ? fmaf(s, e, 1.0f) : s + e;
+    m = up ? t : m;
+}
+
+// Merge of two (max, sum) pairs; (-inf, 0) is the empty pair.
+__device__ __forceinline__ void online_merge(float& m, float& s, float om, float os) {
+    const float M = fmaxf(m, om);
+    if (M == -INFINITY) return;
+    s = (m == -INFINITY ? 0.0f : s * __builtin_amdgcn_exp2f(m - M)) +
+        (om == -INFINITY ? 0.0f : os * __builtin_amdgcn_exp2f(om - M));
+    m = M;
+}
+
+// The 16x16 blocks of one wave's tile.  EDGE: the tile crosses the last row
+// or column, so every store (and every statistic) is bounds-checked.
+template <int WTM, int WTN, int STATS, bool EDGE>
+__device__ __forceinline__ void store_blocks(const GemmArgs& g, const v4f (&acc)[WTN][WTM],
+                                             const float (&sa_reg)[WTM], const float (&sw_reg)[WTN][4], int m0,
+                                             int n0, int wm, int wn, int lane, int split, float (&sm)[WTM],
+                                             float (&ss)[WTM]) {
     const int kg = lane >> 4;
     const int r16 = lane & 15;
-    const int64_t col = (int64_t)nt * WN + wn;
-    // the stored value of output (i, r) of row block j, or -inf past the last column
-    auto zval = [&](int i, int j, int r) {
-        const int n = n0 + (wn * WTN + i) * 16 + 4 * kg + r;
-        const float y = (acc[i][j][r] * sa_reg[j]) * sw_reg[i][r];
-        return n < g.N ? bf16_to_f32(f32_to_bf16_rne(y)) : -INFINITY;
-    };
+    if (STATS == 0 && g.splits > 1) {
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) {
+            const int m = m0 + (wm * WTM + j) * 16 + r16;
+            float* row = g.partial + ((int64_t)split * g.M + m) * g.ldp;
+#pragma unroll
+            for (int i = 0; i < WTN; ++i) {
+                const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
+                if (EDGE && !(n < g.N && m < g.M)) continue;
+                const v4f a = acc[i][j];
+                *reinterpret_cast<float4*>(row + n) = make_float4(a[0], a[1], a[2], a[3]);
+            }
+        }
+        return;
+    }
+    if (STATS == 0 && g.out_f32) {
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) {
+            const int m = m0 + (wm * WTM + j) * 16 + r16;
+            float* row = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy;
+#pragma unroll
+            for (int i = 0; i < WTN; ++i) {
+                const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
+                float y[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) y[r] = (acc[i][j][r] * sa_reg[j]) * sw_reg[i][r];
+                if (!EDGE || n + 3 < g.N) {
+                    if (!EDGE || m < g.M) *reinterpret_cast<float4*>(row + n) = make_float4(y[0], y[1], y[2], y[3]);
+                } else if (m < g.M) {
+                    for (int r = 0; r < 4 && n + r < g.N; ++r) row[n + r] = y[r];
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < WTM; ++j) {
         const int m = m0 + (wm * WTM + j) * 16 + r16;
-        float2 out;
-        if (g.stats_mode == 2) {
-            float bv = -INFINITY;
-            int bi = 0x7fffffff;
+        uint16_t* row = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy;
 #pragma unroll
-            for (int i = 0; i < WTN; ++i)
+        for (int i = 0; i < WTN; ++i) {
+            const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
+            uint32_t bits[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) bits[r] = f32_to_bf16_rne((acc[i][j][r] * sa_reg[j]) * sw_reg[i][r]);
+            if constexpr (STATS == 1) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int n = n0 + (wn * WTN + i) * 16 + 4 * kg + r;
-                    const float v = zval(i, j, r);
-                    if (n < g.N && beats(v, n, bv, bi)) { bv = v; bi = n; }
+                    const float t = bf16_to_f32(bits[r]) * g.c2;
+                    online_add(sm[j], ss[j], (!EDGE || n + r < g.N) ? t : -INFINITY);
                 }
+            } else if constexpr (STATS == 2) {
+                // a lane visits its columns in increasing order, so a strict
+                // comparison keeps the lowest column of a tie
 #pragma unroll
-            for (int o = 16; o <= 32; o <<= 1) {
-                const float ov = __shfl_xor(bv, o, 64);
-                const int oi = __shfl_xor(bi, o, 64);
-                if (beats(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+                for (int r = 0; r < 4; ++r) {
+                    const float z = bf16_to_f32(bits[r]);
+                    const bool gt = (!EDGE || n + r < g.N) && z > sm[j];
+                    sm[j] = gt ? z : sm[j];
+                    ss[j] = gt ? __int_as_float(n + r) : ss[j];
+                }
             }
-            out = make_float2(bv, __int_as_float(bi));
-        } else {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int i = 0; i < WTN; ++i)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, zval(i, j, r));
-            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float M = mx * g.c2;
-            float s = 0.0f;
-            if (M != -INFINITY) {
-#pragma unroll
-                for (int i = 0; i < WTN; ++i)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) s += __builtin_amdgcn_exp2f(fmaf(zval(i, j, r), g.c2, -M));
+            if (!EDGE || n + 3 < g.N) {
+                if (!EDGE || m < g.M) {
+                    uint2 o;
+                    o.x = bits[0] | (bits[1] << 16);
+                    o.y = bits[2] | (bits[3] << 16);
+                    *reinterpret_cast<uint2*>(row + n) = o;
+                }
+            } else if (m < g.M) {
+                for (int r = 0; r < 4 && n + r < g.N; ++r) row[n + r] = (uint16_t)bits[r];
             }
-            s += __shfl_xor(s, 16, 64);
-            s += __shfl_xor(s, 32, 64);
-            out = make_float2(M, s);
         }
-        if (kg == 0 && m < g.M) g.stats[(int64_t)m * g.ld_stats + col] = out;
     }
 }
 
-template <int WTM, int WTN, int WM, int WN, int STAGES, bool STATS>
+// Epilogue: lane holds D[n = 4*(lane/16) + r][m = lane%16] of each 16x16
+// block; the scales were fetched into registers before the main loop.  With a
+// K split the fp32 partial goes to the workspace instead.  Tiles wholly
+// inside the output take the unchecked path.
+//
+// STATS (bf16 output, no K split): the statistics of the stored values of
+// each row over the columns this wave holds (column group nt * WN + wn), for
+// the acceptance test of the logits: STATS 1 keeps (max t, sum 2^(t - max))
+// of t = fl32(z * c2) online while the row's values are stored; STATS 2 keeps
+// (max z, lowest column).  The 4 lanes r16 + 16 kg that share a row are then
+// combined by two xor shuffles in a fixed order.  Empty groups store (-inf,
+// 0) (STATS 1) or (-inf, INT_MAX bits) (STATS 2).
+template <int WTM, int WTN, int WN, int STATS>
+__device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
+                                           const float (&sw_reg)[WTN][4], int m0, int n0, int wm, int wn, int lane,
+                                           int split, int nt, int BM, int BN) {
+    float sm[WTM], ss[WTM];      // STATS 1: running max and sum; STATS 2: best value and (int bits) its column
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) {
+        sm[j] = STATS == 1 ? -FLT_MAX : -INFINITY;
+        ss[j] = STATS == 2 ? __int_as_float(0x7fffffff) : 0.0f;
+    }
+    if (m0 + BM <= g.M && n0 + BN <= g.N)
+        store_blocks<WTM, WTN, STATS, false>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, sm, ss);
+    else
+        store_blocks<WTM, WTN, STATS, true>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, sm, ss);
+    if constexpr (STATS != 0) {
+        const int kg = lane >> 4;
+        const int r16 = lane & 15;
+        const int64_t col = (int64_t)nt * WN + wn;
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) {
+            float m1 = sm[j], s1 = ss[j];
+            if (STATS == 1 && m1 == -FLT_MAX) m1 = -INFINITY;      // no column of this group in this lane
+#pragma unroll
+            for (int o = 16; o <= 32; o <<= 1) {
+                const float m2 = __shfl_xor(m1, o, 64);
+                const float s2 = __shfl_xor(s1, o, 64);
+                if (STATS == 2) {
+                    if (beats(m2, __float_as_int(s2), m1, __float_as_int(s1))) { m1 = m2; s1 = s2; }
+                } else {
+                    online_merge(m1, s1, m2, s2);
+                }
+            }
+            const int m = m0 + (wm * WTM + j) * 16 + r16;
+            if (kg == 0 && m < g.M) g.stats[(int64_t)m * g.ld_stats + col] = make_float2(m1, s1);
+        }
+    }
+}
+
+template <int WTM, int WTN, int WM, int WN, int STAGES, int STATS>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     using C = GemmCfg<WTM, WTN, WM, WN, STAGES>;
     static_assert(STAGES >= 2 && STAGES <= 4, "2..4 stages");
@@ -486,8 +525,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
 #undef SPEC_STEP
     wait_vmcnt<0>();   // no direct-to-LDS write may outlive the workgroup
 
-    store_tile<WTM, WTN>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split);
-    if constexpr (STATS) tile_stats<WTM, WTN, WN>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, nt, lane);
+    store_tile<WTM, WTN, WN, STATS>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, nt, C::BM, C::BN);
 }
 
 // Sum the split-K partials in split order, then scale and convert.
@@ -556,17 +594,26 @@ constexpr int kCfgBM[kKinds] = {Cfg0::BM, Cfg1::BM, Cfg2::BM, Cfg3::BM, Cfg4::BM
 constexpr int kCfgBN[kKinds] = {Cfg0::BN, Cfg1::BN, Cfg2::BN, Cfg3::BN, Cfg4::BN, Cfg5::BN, Cfg6::BN, Cfg7::BN, Cfg8::BN};
 constexpr int kCfgWN[kKinds] = {2, 2, 2, 2, 2, 2, 1, 2, 2};   // waves across N (statistics groups per tile)
 
-// The statistics epilogue is a separate instantiation, so the plain GEMMs'
-// register allocation does not carry it.
-template <class C, int WTM, int WTN, int WM, int WN, int STAGES>
+// The statistics epilogues are separate instantiations, so the plain GEMMs'
+// register allocation does not carry them (and the 160x224 tile, whose
+// statistics variant would spill, has none: the plan never asks for it).
+template <class C, int WTM, int WTN, int WM, int WN, int STAGES, bool WITH_STATS = true>
 hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
     const int total = g.m_tiles * g.n_tiles * g.splits;
-    if (g.stats_mode != 0)
-        hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, true>), dim3(total), dim3(C::kThreads), 0,
-                           stream, g);
-    else
-        hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, false>), dim3(total), dim3(C::kThreads), 0,
-                           stream, g);
+    if constexpr (WITH_STATS) {
+        if (g.stats_mode == 1) {
+            hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 1>), dim3(total), dim3(C::kThreads), 0,
+                               stream, g);
+            return hipGetLastError();
+        }
+        if (g.stats_mode == 2) {
+            hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 2>), dim3(total), dim3(C::kThreads), 0,
+                               stream, g);
+            return hipGetLastError();
+        }
+    }
+    if (g.stats_mode != 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 0>), dim3(total), dim3(C::kThreads), 0, stream, g);
     return hipGetLastError();
 }
 
@@ -645,7 +692,7 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
     switch (p.kind) {
         case 0: e = launch_cfg<Cfg0, 2, 2, 2, 2, 4>(g, stream); break;
         case 1: e = launch_cfg<Cfg1, 5, 4, 1, 2, 4>(g, stream); break;
-        case 2: e = launch_cfg<Cfg2, 5, 7, 2, 2, 3>(g, stream); break;
+        case 2: e = launch_cfg<Cfg2, 5, 7, 2, 2, 3, false>(g, stream); break;
         case 3: e = launch_cfg<Cfg3, 8, 4, 2, 2, 3>(g, stream); break;
         case 4: e = launch_cfg<Cfg4, 5, 6, 2, 2, 3>(g, stream); break;
         case 5: e = launch_cfg<Cfg5, 5, 4, 2, 2, 4>(g, stream); break;
