@@ -244,6 +244,56 @@ spec_status spec_verify_accept_stats(const void* target_logits, const float* tar
                                      int32_t* out_tokens, int32_t* num_accepted,
                                      void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * spec_verify_accept_tree -- acceptance of B drafted token TREES, the
+ * standard EAGLE drafting mode the paper compares with greedy chains (the
+ * appendix's tree versus greedy drafting; Table 2's tree rows).  The target
+ * scored every node in one pass (tree attention, outside this library).
+ *
+ * Tree of sequence b: N nodes; parents[b,n] in [-1, n) is node n's parent (-1:
+ * a candidate for the first new token); tokens[b,n] its drafted token.  The
+ * children of a node are its candidates, in index order.  Target row 0 scores
+ * the first new position, row n+1 the position after node n.
+ *
+ *   temperature == 0: from the root, move to the first child whose token is
+ *     the argmax of the current row (lowest index on ties); where none
+ *     matches, emit that argmax.
+ *   temperature > 0: the candidates are deterministic proposals (one-hot
+ *     draft distributions, e.g. a top-k expansion).  With P = softmax(row/T)
+ *     at the current node, child n (token x) is accepted iff
+ *     u[b,n] * (1 - S) < P(x), S the mass of the tokens already rejected at
+ *     this node (a repeated token has P = 0); on acceptance the walk moves to
+ *     n, else x is removed.  Where every child is rejected (or there is none),
+ *     emit the smallest v whose cumulative sum of P without the removed
+ *     tokens exceeds u[b,N] times that residual's total (P itself if the
+ *     residual vanished).  This is sequential sampling from P: the emitted
+ *     tokens follow the target distribution exactly.  With parents = [-1, 0,
+ *     .., N-2] it is spec_verify_accept with draft_logits NULL and k = N.
+ *
+ * target_logits  bf16 [B, N+1, V].
+ * parents, tokens int32 [B, N]; a node whose parent is outside [-1, n) is never
+ *                accepted; a token outside [0, V) is a rejection with P = 0.
+ * uniforms       fp32 [B, N+1] in [0, 1): u[b,n] tests node n, u[b,N] is the final
+ *                draw (ignored when temperature == 0).
+ * out_tokens     int32 [B, N+1]: the accepted path's tokens, then the emitted token,
+ *                -1 padded.
+ * accepted_nodes int32 [B, N]: the accepted path's node indices, -1 padded.
+ * num_accepted   int32 [B]: path length a_b; a_b + 1 tokens are emitted.
+ * workspace      >= spec_verify_accept_tree_workspace_bytes(B, N, V); contents on entry
+ *                are ignored.
+ * Requirements: B >= 0 (0 is a no-op), 1 <= N <= 64, 1 <= V <= 2^22, B <= 65535
+ * (SPEC_ERR_UNSUPPORTED otherwise); temperature finite and >= 0 (SPEC_ERR_VALUE).
+ * Probabilities are computed in fp32 (the accept tests in double from fp32
+ * statistics); a decision within ~1e-5 relative of its boundary may differ from
+ * an exact evaluation.
+ */
+size_t spec_verify_accept_tree_workspace_bytes(int64_t B, int64_t N, int64_t V);
+
+spec_status spec_verify_accept_tree(const void* target_logits, const int32_t* parents, const int32_t* tokens,
+                                    const float* uniforms, int64_t B, int64_t N, int64_t V, float temperature,
+                                    int32_t* out_tokens, int32_t* accepted_nodes, int32_t* num_accepted,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* spec_status_string(spec_status s);
 

@@ -21,6 +21,8 @@ from .ops import (  # noqa: F401
     logit_stats_count,
     verify_accept,
     accept_workspace_bytes,
+    verify_accept_tree,
+    accept_tree_workspace_bytes,
 )
 
 __version__ = "0.1.0"

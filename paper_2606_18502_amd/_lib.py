@@ -20,6 +20,7 @@ OUT_BF16, OUT_F32 = 0, 1
 EXPORTS = ("spec_fp8_quantize", "spec_silu_mul_bf16", "spec_fp8_gemm_workspace_bytes", "spec_fp8_gemm",
            "spec_logit_stats_count", "spec_fp8_gemm_logit_stats",
            "spec_verify_accept_workspace_bytes", "spec_verify_accept", "spec_verify_accept_stats",
+           "spec_verify_accept_tree_workspace_bytes", "spec_verify_accept_tree",
            "spec_status_string", "spec_last_hip_error", "spec_version")
 
 _lib = None
@@ -58,6 +59,10 @@ def load() -> ctypes.CDLL:
     lib.spec_fp8_gemm_logit_stats.restype = i32
     lib.spec_verify_accept_stats.argtypes = [vp, vp, i64, i64, vp, vp, vp, i64, i64, i64, f32, vp, vp, vp, sz, vp]
     lib.spec_verify_accept_stats.restype = i32
+    lib.spec_verify_accept_tree_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.spec_verify_accept_tree_workspace_bytes.restype = sz
+    lib.spec_verify_accept_tree.argtypes = [vp, vp, vp, vp, i64, i64, i64, f32, vp, vp, vp, vp, sz, vp]
+    lib.spec_verify_accept_tree.restype = i32
     lib.spec_verify_accept_workspace_bytes.argtypes = [i64, i64, i64]
     lib.spec_verify_accept_workspace_bytes.restype = sz
     lib.spec_verify_accept.argtypes = [vp, vp, vp, vp, i64, i64, i64, f32, vp, vp, vp, sz, vp]

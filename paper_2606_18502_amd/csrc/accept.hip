@@ -48,6 +48,8 @@ struct AcceptArgs {
     const float* u;
     int32_t* out;
     int32_t* num;
+    const int32_t* parent; // token tree: parent node of each node, -1 for the root's candidates (tree mode)
+    int32_t* nodes;        // token tree: accepted node indices [B][k] (tree mode)
     float2* stats;         // [B][Rs][nslice] statistics of the streamed rows
     const float2* tst;     // target rows' statistics from the LM-head epilogue, or null
     int64_t ldtst;         // row stride of tst (entries)
@@ -298,7 +300,14 @@ struct Dist {
     float mt, inv_zt;         // merged max and 1/sum of the target row
     float md, inv_zd;
     int64_t skip;             // element forced to zero (one-hot draft), -1 if none
+    int64_t kill0;            // token tree: bit i of `kill` zeroes element kill0 + i (rejected candidates)
+    uint64_t kill;
 };
+
+__device__ __forceinline__ bool killed(const Dist& d, int64_t e) {
+    const uint64_t i = (uint64_t)(e - d.kill0);
+    return i < 64 && ((d.kill >> i) & 1ull);
+}
 
 // Probabilities of the 8 elements at e (< e1) from loaded vectors: with a
 // draft row (HAS_D) the residual max(0, p - q), else p with element `skip`
@@ -321,7 +330,7 @@ __device__ __forceinline__ void dist8(const Dist& d, float c2, const uint4& rt, 
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             const float p = __builtin_amdgcn_exp2f(fmaf(zt[q], c2, -d.mt)) * d.inv_zt;
-            r[q] = (in8<VEC>(e, q, e1) && e + q != d.skip) ? p : 0.0f;
+            r[q] = (in8<VEC>(e, q, e1) && e + q != d.skip && !killed(d, e + q)) ? p : 0.0f;
         }
     }
 }
@@ -334,7 +343,7 @@ __device__ __forceinline__ float dist1(const Dist& d, float c2, int64_t e) {
         const float qq = __builtin_amdgcn_exp2f(fmaf(bf16_to_f32(d.zd_row[e]), c2, -d.md)) * d.inv_zd;
         return fmaxf(p - qq, 0.0f);
     } else {
-        return e != d.skip ? p : 0.0f;
+        return (e != d.skip && !killed(d, e)) ? p : 0.0f;
     }
 }
 
@@ -533,6 +542,8 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     d.md = 0.0f;
     d.inv_zd = 0.0f;
     d.skip = -1;
+    d.kill0 = 0;
+    d.kill = 0;
     if (j < k) {
         if (a.zd) {
             d.zd_row = a.zd + ((int64_t)b * k + j) * a.V;
@@ -641,6 +652,288 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     }
 }
 
+// ------------------------------------------------------------- token tree
+//
+// Tree mode: the N drafted nodes of a sequence form a tree (parent[n] in
+// [-1, n), -1 for candidates of the first new position); target row 0 scores
+// the first new position and row n+1 the position after node n, so a
+// sequence has N+1 target rows, whose statistics the streaming kernels above
+// compute as for k = N.  The children of a node are its candidates, tested
+// in index order.  A node whose parent is out of range is never reached.
+
+constexpr int kMaxTree = 64;   // nodes per sequence
+
+// Merged (max logit, lowest index) of row r of sequence b, for lanes of one wave.
+__device__ __forceinline__ int merged_argmax(const AcceptArgs& a, int b, int r, int lane) {
+    uint32_t nst;
+    const float2* st = row_stats(a, b, r, nst);
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int64_t c0 = lane; c0 < nst; c0 += 8 * 64) {
+        float2 pv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int64_t c = c0 + q * 64;
+            pv[q] = c < nst ? st[c] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int pi = __float_as_int(pv[q].y);
+            if (better(pv[q].x, pi, bv, bi)) { bv = pv[q].x; bi = pi; }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    return bi;
+}
+
+// Writes sequence b's outputs: the tokens of the accepted path, then the
+// emitted token, -1 padded to N+1; the path's node indices, -1 padded to N.
+__device__ __forceinline__ void tree_outputs(const AcceptArgs& a, int b, const int* path, const int* x, int depth,
+                                             int token, int i0, int step) {
+    const int N = a.k;
+    for (int i = i0; i <= N; i += step) {
+        a.out[(int64_t)b * (N + 1) + i] = i < depth ? x[path[i]] : (i == depth ? token : -1);
+        if (i < N) a.nodes[(int64_t)b * N + i] = i < depth ? path[i] : -1;
+    }
+}
+
+// Greedy walk (one block per sequence): the argmax of every row from its
+// slice statistics, then from the root the first child whose token is the
+// current row's argmax, until no child matches; that argmax is emitted.
+__global__ __launch_bounds__(256) void tree_greedy_kernel(AcceptArgs a) {
+    __shared__ int g[kMaxTree + 1];
+    __shared__ int s_par[kMaxTree], s_x[kMaxTree], s_path[kMaxTree];
+    __shared__ int s_depth, s_tok;
+    const int b = blockIdx.x;
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    const int N = a.k;
+    if (t < N) {
+        s_par[t] = a.parent[(int64_t)b * N + t];
+        s_x[t] = a.x[(int64_t)b * N + t];
+    }
+    for (int r = wv; r <= N; r += 4) {
+        const int bi = merged_argmax(a, b, r, lane);
+        if (lane == 0) g[r] = bi;
+    }
+    __syncthreads();
+    if (t == 0) {
+        int cur = -1, depth = 0;
+        for (;;) {
+            const int gv = g[cur + 1];
+            int nxt = -1;
+            for (int n = cur + 1; n < N; ++n)
+                if (s_par[n] == cur && s_x[n] == gv) { nxt = n; break; }
+            if (nxt < 0) break;
+            s_path[depth++] = nxt;
+            cur = nxt;
+        }
+        s_depth = depth;
+        s_tok = g[cur + 1];
+    }
+    __syncthreads();
+    tree_outputs(a, b, s_path, s_x, s_depth, s_tok, t, blockDim.x);
+    if (t == 0) a.num[b] = s_depth;
+}
+
+// Sampling walk, block (chunk c, sequence b).  Every block merges the row
+// statistics, gets every candidate's target probability in parallel (one
+// round trip for all of them) and walks the tree identically: at the current
+// node, child n with token x is accepted iff u[n] (1 - S) < P(x), S the mass
+// of the tokens already rejected there (a repeated token has P = 0); on
+// acceptance the walk moves to n, else x is removed.  Where every child is
+// rejected (or there is none) the final draw comes from P with the removed
+// tokens zeroed: each block sums its chunk as for chains (the removed tokens
+// of a 64-element range are a bit mask), and the last block of the sequence
+// searches the chunk, the range and the element holding u[N] R.
+template <bool VEC>
+__global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
+    __shared__ float sM[kMaxTree + 1], sZ[kMaxTree + 1];
+    __shared__ int s_par[kMaxTree], s_x[kMaxTree], s_path[kMaxTree], s_kill[kMaxTree];
+    __shared__ double s_p[kMaxTree];
+    __shared__ float s_u[kMaxTree + 1];
+    __shared__ int s_f, s_depth, s_nkill, s_last;
+    __shared__ double sh[kWavesPerBlock];
+    __shared__ int s_own, s_lastpos;
+    __shared__ double s_base;
+    const int64_t c = blockIdx.x;
+    const int b = blockIdx.y;
+    const int t = threadIdx.x;
+    const int lane = t & 63, wv = t >> 6;
+    const int N = a.k;
+
+    // the tree, the uniforms and the candidates' logits are loaded first, so
+    // their round trips overlap the statistics merge
+    int par = -2, xv = -1;
+    float zx = 0.0f;
+    bool ok = false;
+    if (t < N) {
+        par = a.parent[(int64_t)b * N + t];
+        xv = a.x[(int64_t)b * N + t];
+        s_par[t] = par;
+        s_x[t] = xv;
+        ok = par >= -1 && par < t && xv >= 0 && xv < a.V;
+        if (ok) zx = bf16_to_f32(a.zt[((int64_t)b * (N + 1) + par + 1) * a.V + xv]);
+    }
+    if (t <= N) s_u[t] = a.u[(int64_t)b * (N + 1) + t];
+    for (int r = wv; r <= N; r += kWavesPerBlock) {
+        uint32_t nst;
+        const float2* st = row_stats(a, b, r, nst);
+        float m = -INFINITY, z = 0.0f;
+        for (int64_t q0 = lane; q0 < nst; q0 += 8 * kWave) {
+            float2 v[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int64_t qi = q0 + q * kWave;
+                v[q] = qi < nst ? st[qi] : make_float2(-INFINITY, 0.0f);
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) merge_ms(m, z, v[q].x, v[q].y);
+        }
+        const float M = wave_max(m);
+        const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));
+        if (lane == 0) { sM[r] = M; sZ[r] = Z; }
+    }
+    __syncthreads();
+    // every candidate's probability under its parent's row; t - M is formed
+    // exactly in double (bf16 * fp32 fits in 53 bits), as for chains
+    if (t < N) s_p[t] = ok ? exp2((double)zx * (double)a.c2 - (double)sM[par + 1]) / (double)sZ[par + 1] : 0.0;
+    __syncthreads();
+    if (t == 0) {
+        int cur = -1, depth = 0, nk = 0;
+        for (;;) {
+            double S = 0.0;
+            int nxt = -1;
+            nk = 0;
+            for (int n = cur + 1; n < N; ++n) {
+                if (s_par[n] != cur) continue;
+                const int x = s_x[n];
+                bool valid = x >= 0 && x < a.V;
+                for (int i = 0; i < nk && valid; ++i) valid = s_kill[i] != x;
+                const double px = valid ? s_p[n] : 0.0;
+                if ((double)s_u[n] * (1.0 - S) < px) { nxt = n; break; }
+                if (valid) {
+                    s_kill[nk++] = x;
+                    S += px;
+                }
+            }
+            if (nxt < 0) break;
+            s_path[depth++] = nxt;
+            cur = nxt;
+        }
+        s_f = cur;
+        s_depth = depth;
+        s_nkill = nk;
+    }
+    __syncthreads();
+    const int f = s_f;
+    int nk = s_nkill;
+
+    Dist d;
+    d.zt_row = a.zt + ((int64_t)b * (N + 1) + f + 1) * a.V;
+    d.mt = sM[f + 1];
+    d.inv_zt = 1.0f / sZ[f + 1];
+    d.zd_row = nullptr;
+    d.md = 0.0f;
+    d.inv_zd = 0.0f;
+    d.skip = -1;
+    auto killed_in = [&](int64_t e0, Dist& dd) {     // the removed tokens of the range [e0, e0 + 64)
+        dd.kill0 = e0;
+        dd.kill = 0;
+        for (int i = 0; i < nk; ++i) {
+            const uint64_t off = (uint64_t)((int64_t)s_kill[i] - e0);
+            if (off < 64) dd.kill |= 1ull << off;
+        }
+    };
+    double* cm = a.chunkm + (int64_t)b * a.nchunk;
+    double* fm = a.finem + (int64_t)b * a.nchunk * kAThreads;
+    auto range_of = [&](int64_t ch, int th, int64_t& e0, int64_t& e1) {
+        e0 = ch * kChunk + (int64_t)th * kPerThread;
+        e1 = min(e0 + kPerThread, a.V);
+    };
+    auto mass_of = [&](int64_t ch) {
+        int64_t e0, e1;
+        range_of(ch, t, e0, e1);
+        if (e0 >= a.V) return 0.0;
+        Dist dd = d;
+        killed_in(e0, dd);
+        return range_mass<VEC, false>(dd, a.c2, e0, e1);
+    };
+    {
+        const double m = mass_of(c);
+        store_coherent(fm + c * kAThreads + t, m);
+        double lo, hi, tot;
+        block_scan_d(m, sh, lo, hi, tot);
+        if (t == 0) store_coherent(cm + c, tot);
+        wait_stores();
+        __syncthreads();
+        if (t == 0) {
+            const unsigned int ticket = __hip_atomic_fetch_add(a.ctr + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_last = (ticket == (unsigned int)(a.nchunk - 1));
+        }
+        __syncthreads();
+        if (!s_last) return;
+    }
+    double v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
+    double lo1, hi1, R;
+    block_scan_d(v1, sh, lo1, hi1, R);
+    if (!(R > 0.0)) {
+        // the removed tokens held all the mass: draw from P itself
+        nk = 0;
+        for (int64_t ch = 0; ch < a.nchunk; ++ch) {
+            const double m = mass_of(ch);
+            store_coherent(fm + ch * kAThreads + t, m);
+            double lo, hi, tot;
+            block_scan_d(m, sh, lo, hi, tot);
+            if (t == 0) store_coherent(cm + ch, tot);
+        }
+        wait_stores();
+        __syncthreads();
+        v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
+        block_scan_d(v1, sh, lo1, hi1, R);
+    }
+    const double target = (double)s_u[N] * R;
+    find_owner(v1, lo1, hi1, 0.0, target, &s_own, &s_base, &s_lastpos);
+    const int64_t cs = s_own;
+    const double base2 = s_base;
+    const double v2 = load_coherent(fm + cs * kAThreads + t);
+    double lo2, hi2, tot2;
+    block_scan_d(v2, sh, lo2, hi2, tot2);
+    find_owner(v2, lo2, hi2, base2, target, &s_own, &s_base, &s_lastpos);
+    if (wv == 0) {
+        int64_t e0, e1;
+        range_of(cs, s_own, e0, e1);
+        const double base3 = s_base;
+        Dist dd = d;
+        killed_in(e0, dd);
+        const int64_t e = e0 + lane;
+        const float r = e < e1 ? dist1<false>(dd, a.c2, e) : 0.0f;
+        double incl = (double)r;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const double y = __shfl_up(incl, o, kWave);
+            if (lane >= o) incl += y;
+        }
+        double excl = __shfl_up(incl, 1, kWave);
+        if (lane == 0) excl = 0.0;
+        const unsigned long long own = __ballot(base3 + excl <= target && target < base3 + incl);
+        const unsigned long long pos = __ballot(r > 0.0f);
+        int pick;
+        if (own) pick = __ffsll((long long)own) - 1;
+        else if (pos) pick = 63 - __builtin_clzll(pos);
+        else pick = 0;
+        tree_outputs(a, b, s_path, s_x, s_depth, (int)min(e0 + pick, a.V - 1), lane, kWave);
+        if (lane == 0) {
+            a.num[b] = s_depth;
+            a.ctr[b] = 0u;
+        }
+    }
+}
+
 // Clears the sample kernel's tickets when no statistics kernel runs (target
 // statistics given and no draft logits to stream).
 __global__ __launch_bounds__(256) void clear_tickets_kernel(unsigned int* ctr, int n) {
@@ -672,7 +965,7 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
                          const float* u, int64_t B, int64_t k, int64_t V, float temperature,
                          int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream,
                          const float2* tstats, int64_t n_tstats, int64_t ld_tstats) {
-    AcceptArgs a;
+    AcceptArgs a{};
     a.tst = tstats; a.ntst = (uint32_t)n_tstats; a.ldtst = ld_tstats;
     char* ws = reinterpret_cast<char*>(workspace);
     a.zt = zt; a.zd = zd; a.x = x; a.u = u; a.out = out_tokens; a.num = num_accepted;
@@ -715,6 +1008,45 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
     dim3 g2((unsigned)p.nchunk, (unsigned)B);
     if (vec) hipLaunchKernelGGL(stoch_sample_kernel<true>, g2, dim3(kAThreads), 0, stream, a);
     else hipLaunchKernelGGL(stoch_sample_kernel<false>, g2, dim3(kAThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int32_t* parent, const int32_t* x,
+                              const float* u, int64_t B, int64_t N, int64_t V, float temperature,
+                              int32_t* out_tokens, int32_t* accepted_nodes, int32_t* num_accepted, void* workspace,
+                              hipStream_t stream) {
+    AcceptArgs a{};
+    char* ws = reinterpret_cast<char*>(workspace);
+    a.zt = zt; a.zd = nullptr; a.x = x; a.u = u; a.out = out_tokens; a.num = num_accepted;
+    a.parent = parent; a.nodes = accepted_nodes;
+    a.stats = reinterpret_cast<float2*>(ws + p.stats_off);
+    a.chunkm = reinterpret_cast<double*>(ws + p.mass_off);
+    a.finem = reinterpret_cast<double*>(ws + p.fine_off);
+    a.ctr = reinterpret_cast<unsigned int*>(ws + p.ctr_off);
+    a.tst = nullptr; a.ntst = 0; a.ldtst = 0;
+    a.V = V; a.nchunk = p.nchunk; a.nslice = (uint32_t)p.nschunk; a.B = (int)B; a.k = (int)N;
+    a.R = a.Rs = (uint32_t)(N + 1);
+    a.rt0 = 0;
+    a.items = (uint32_t)(B * a.Rs * p.nschunk);
+    const bool vec = (V % 8 == 0) && ((uintptr_t)zt % 16 == 0);
+    const unsigned g1 = (unsigned)((stream_waves(a.items) + kWavesPerBlock - 1) / kWavesPerBlock);
+    if (temperature == 0.0f) {
+        a.c2 = 0.0f;
+        if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
+        else hipLaunchKernelGGL(greedy_partial_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(tree_greedy_kernel, dim3((unsigned)B), dim3(256), 0, stream, a);
+        return hipGetLastError();
+    }
+    a.c2 = (float)(1.4426950408889634 / (double)temperature);
+    if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
+    else hipLaunchKernelGGL(stoch_stats_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 g2((unsigned)p.nchunk, (unsigned)B);
+    if (vec) hipLaunchKernelGGL(tree_sample_kernel<true>, g2, dim3(kAThreads), 0, stream, a);
+    else hipLaunchKernelGGL(tree_sample_kernel<false>, g2, dim3(kAThreads), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -126,6 +126,26 @@ spec_status spec_verify_accept_stats(const void* target_logits, const float* tar
                                            n_stats, ld_stats));
 }
 
+size_t spec_verify_accept_tree_workspace_bytes(int64_t B, int64_t N, int64_t V) {
+    if (B <= 0 || N < 1 || V < 1) return 0;
+    return specfp8::plan_accept(B, N, V).bytes;
+}
+
+spec_status spec_verify_accept_tree(const void* target_logits, const int32_t* parents, const int32_t* tokens,
+                                    const float* uniforms, int64_t B, int64_t N, int64_t V, float temperature,
+                                    int32_t* out_tokens, int32_t* accepted_nodes, int32_t* num_accepted,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+    const spec_status st = specfp8::check_accept_tree(target_logits, parents, tokens, uniforms, B, N, V, temperature,
+                                                      out_tokens, accepted_nodes, num_accepted);
+    if (st != SPEC_OK || B == 0) return st;
+    const specfp8::AcceptPlan plan = specfp8::plan_accept(B, N, V);
+    if (!workspace || workspace_bytes < plan.bytes) return SPEC_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return SPEC_ERR_ALIGN;
+    return from_hip(specfp8::launch_accept_tree(plan, reinterpret_cast<const uint16_t*>(target_logits), parents,
+                                                tokens, uniforms, B, N, V, temperature, out_tokens, accepted_nodes,
+                                                num_accepted, workspace, as_stream(stream)));
+}
+
 const char* spec_status_string(spec_status s) {
     switch (s) {
         case SPEC_OK: return "ok";
@@ -143,6 +163,6 @@ const char* spec_status_string(spec_status s) {
 
 int spec_last_hip_error(void) { return g_last_hip_error; }
 
-int spec_version(void) { return 200; }
+int spec_version(void) { return 300; }
 
 }  // extern "C"

@@ -49,4 +49,11 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
                          int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream,
                          const float2* tstats = nullptr, int64_t n_tstats = 0, int64_t ld_tstats = 0);
 
+// Token-tree verification (N nodes per sequence, N+1 target rows); the plan
+// is plan_accept(B, N, V).
+hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int32_t* parent, const int32_t* x,
+                              const float* u, int64_t B, int64_t N, int64_t V, float temperature,
+                              int32_t* out_tokens, int32_t* accepted_nodes, int32_t* num_accepted, void* workspace,
+                              hipStream_t stream);
+
 }  // namespace specfp8

@@ -85,6 +85,25 @@ spec_status check_accept_stats(const float* target_stats, int64_t n_stats, int64
     return SPEC_OK;
 }
 
+spec_status check_accept_tree(const void* target_logits, const int32_t* parents, const int32_t* tokens,
+                              const float* uniforms, int64_t B, int64_t N, int64_t V, float temperature,
+                              const int32_t* out_tokens, const int32_t* accepted_nodes,
+                              const int32_t* num_accepted) {
+    if (!isfinite(temperature) || temperature < 0.0f) return SPEC_ERR_VALUE;
+    if (B < 0 || N < 1 || V < 1) return SPEC_ERR_SHAPE;
+    if (N > 64 || V > 4194304LL || B > kMaxGridY) return SPEC_ERR_UNSUPPORTED;
+    if (B == 0) return SPEC_OK;
+    if (!target_logits || !parents || !tokens || !out_tokens || !accepted_nodes || !num_accepted)
+        return SPEC_ERR_NULL;
+    if (temperature > 0.0f && !uniforms) return SPEC_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(target_logits) & 1u) return SPEC_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(parents) & 3u) || (reinterpret_cast<uintptr_t>(tokens) & 3u) ||
+        (reinterpret_cast<uintptr_t>(out_tokens) & 3u) || (reinterpret_cast<uintptr_t>(accepted_nodes) & 3u) ||
+        (reinterpret_cast<uintptr_t>(num_accepted) & 3u) || (uniforms && (reinterpret_cast<uintptr_t>(uniforms) & 3u)))
+        return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
 spec_status check_accept(const void* target_logits, const void* draft_logits, const int32_t* draft_tokens,
                          const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
                          const int32_t* out_tokens, const int32_t* num_accepted) {

@@ -20,6 +20,10 @@ spec_status check_gemm(const void* a, int64_t lda, const float* a_scale, int a_m
 spec_status check_logit_stats(int64_t M, int64_t V, float temperature, const void* logits, int64_t ld_logits,
                               const float* stats, int64_t ld_stats, int64_t n_groups);
 spec_status check_accept_stats(const float* target_stats, int64_t n_stats, int64_t ld_stats, int64_t B);
+spec_status check_accept_tree(const void* target_logits, const int32_t* parents, const int32_t* tokens,
+                              const float* uniforms, int64_t B, int64_t N, int64_t V, float temperature,
+                              const int32_t* out_tokens, const int32_t* accepted_nodes,
+                              const int32_t* num_accepted);
 spec_status check_accept(const void* target_logits, const void* draft_logits, const int32_t* draft_tokens,
                          const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
                          const int32_t* out_tokens, const int32_t* num_accepted);

@@ -258,3 +258,49 @@ def verify_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tens
             num_accepted.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
             _stream()))
     return out_tokens, num_accepted
+
+
+def accept_tree_workspace_bytes(B: int, N: int, V: int) -> int:
+    return int(_lib.load().spec_verify_accept_tree_workspace_bytes(B, N, V))
+
+
+def verify_accept_tree(target_logits: torch.Tensor, parents: torch.Tensor, tokens: torch.Tensor,
+                       uniforms: Optional[torch.Tensor], temperature: float,
+                       workspace: Optional[torch.Tensor] = None, out_tokens: Optional[torch.Tensor] = None,
+                       accepted_nodes: Optional[torch.Tensor] = None, num_accepted: Optional[torch.Tensor] = None
+                       ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Token-tree acceptance (spec_verify_accept_tree).
+
+    target_logits bf16 [B,N+1,V]; parents, tokens int32 [B,N]; uniforms fp32 [B,N+1] (T>0).
+    Returns (out_tokens int32 [B,N+1], accepted_nodes int32 [B,N], num_accepted int32 [B]).
+    """
+    lib = _lib.load()
+    _dev(target_logits, torch.bfloat16, "target_logits")
+    B, N1, V = target_logits.shape
+    N = N1 - 1
+    if not target_logits.is_contiguous():
+        raise ValueError("target_logits must be contiguous")
+    for name, t in (("parents", parents), ("tokens", tokens)):
+        _dev(t, torch.int32, name)
+        if tuple(t.shape) != (B, N) or not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous [B,N]")
+    if uniforms is not None:
+        _dev(uniforms, torch.float32, "uniforms")
+        if tuple(uniforms.shape) != (B, N1) or not uniforms.is_contiguous():
+            raise ValueError("uniforms must be contiguous [B,N+1]")
+    dev = target_logits.device
+    if out_tokens is None:
+        out_tokens = torch.empty((B, N1), dtype=torch.int32, device=dev)
+    if accepted_nodes is None:
+        accepted_nodes = torch.empty((B, N), dtype=torch.int32, device=dev)
+    if num_accepted is None:
+        num_accepted = torch.empty((B,), dtype=torch.int32, device=dev)
+    need = accept_tree_workspace_bytes(B, N, V)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
+    check("spec_verify_accept_tree", lib.spec_verify_accept_tree(
+        target_logits.data_ptr(), parents.data_ptr(), tokens.data_ptr(),
+        None if uniforms is None else uniforms.data_ptr(), B, N, V, float(temperature), out_tokens.data_ptr(),
+        accepted_nodes.data_ptr(), num_accepted.data_ptr(), workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(), _stream()))
+    return out_tokens, accepted_nodes, num_accepted

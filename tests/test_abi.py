@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.spec_version() == 200
+    assert lib.spec_version() == 300
     for s in range(9):
         assert lib.spec_status_string(s)
     assert lib.spec_status_string(99) == b"unknown status"
@@ -201,3 +201,31 @@ def test_accept_stats_validation(lib):
     assert accs(lib, ws=None) == WS
     assert accs(lib, B=0, zt=None, ts=None, zd=None, x=None, u=None, out=None, num=None, ws=None, wsb=0) == OK
     assert accs(lib, T=0.0, u=None, zd=None, ws=None) == WS             # greedy: no uniforms, no draft logits
+
+
+def tr(lib, zt=A16, par=A16, tok=A16, u=A16, B=2, N=5, V=256, T=0.7, out=A16, nodes=A16, num=A16, ws=A16,
+       wsb=1 << 20):
+    return lib.spec_verify_accept_tree(zt, par, tok, u, B, N, V, ctypes.c_float(T), out, nodes, num, ws, wsb, None)
+
+
+def test_accept_tree_validation(lib):
+    assert tr(lib, T=float("nan")) == VALUE
+    assert tr(lib, T=-1.0) == VALUE
+    assert tr(lib, N=0) == SHAPE
+    assert tr(lib, B=-1) == SHAPE
+    assert tr(lib, V=0) == SHAPE
+    assert tr(lib, N=65) == UNSUP
+    assert tr(lib, V=(1 << 22) + 8) == UNSUP
+    assert tr(lib, B=70000) == UNSUP
+    assert tr(lib, par=None) == NULL
+    assert tr(lib, tok=None) == NULL
+    assert tr(lib, nodes=None) == NULL
+    assert tr(lib, u=None) == NULL                  # T > 0 needs uniforms
+    assert tr(lib, T=0.0, u=None, ws=None) == WS     # greedy needs none
+    assert tr(lib, zt=A1) == ALIGN
+    assert tr(lib, par=A16 + 2) == ALIGN
+    need = lib.spec_verify_accept_tree_workspace_bytes(2, 5, 256)
+    assert need > 0
+    assert tr(lib, wsb=need - 1) == WS
+    assert tr(lib, ws=A16 + 8, wsb=need) == ALIGN
+    assert tr(lib, B=0, zt=None, par=None, tok=None, u=None, out=None, nodes=None, num=None, ws=None, wsb=0) == OK

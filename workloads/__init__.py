@@ -17,5 +17,7 @@ from .gen import (  # noqa: F401
     draft_tokens_greedy,
     draft_tokens_sampled,
     philox_uniforms,
+    tree_shape,
+    tree_tokens_topk,
 )
-from .configs import CONFIGS, C4_CORRELATION  # noqa: F401
+from .configs import CONFIGS, C4_CORRELATION, TREE25  # noqa: F401

@@ -20,6 +20,16 @@ VOCAB = 128256
 # calls only the CPU oracle.
 C4_CORRELATION = 0.9995
 
+# A 25-node draft tree in the style of an EAGLE top-k expansion: 4 candidates
+# for the first new token, the higher-ranked branches expanded deeper (depth
+# 6 along the top branch).  parent[n] of node n; -1 is the root.
+TREE25 = (-1, -1, -1, -1,            # 0-3: first-position candidates
+          0, 0, 0, 1, 1, 2, 3,       # 4-10
+          4, 4, 4, 5, 7,             # 11-15
+          11, 11, 12, 14,            # 16-19
+          16, 16, 18,                # 20-22
+          20, 20)                    # 23-24
+
 # The four linears of one decoder layer: (name, N, K) with W [N,K].
 LAYER_LINEARS = (
     ("qkv", QKV_OUT, HIDDEN),

@@ -140,3 +140,46 @@ def draft_tokens_sampled(zd_bits: np.ndarray, temperature: float, seed: int = 8)
 def philox_uniforms(shape, seed: int = 7) -> np.ndarray:
     """Uniforms in [0,1) as fp32 from Philox(seed)."""
     return _rng(seed).random(shape, dtype=np.float32)
+
+
+def tree_shape(N: int, branching) -> np.ndarray:
+    """Parents [N] of a breadth-first token tree: a node at depth d gets
+    branching[d] children (the last entry repeats) until N nodes exist; -1 is
+    the root (the last accepted token)."""
+    parent = []
+    frontier = [(-1, 0)]
+    while frontier and len(parent) < N:
+        nxt = []
+        for p, d in frontier:
+            k = branching[min(d, len(branching) - 1)]
+            for _ in range(k):
+                if len(parent) == N:
+                    break
+                parent.append(p)
+                nxt.append((len(parent) - 1, d + 1))
+        frontier = nxt
+    return np.asarray(parent, dtype=np.int32)
+
+
+def tree_tokens_topk(zd_bits: np.ndarray, parent: np.ndarray) -> np.ndarray:
+    """Candidate tokens of a top-k tree expansion: the children of node p (in
+    index order) are k highest-scoring tokens of draft row p+1 (which of
+    several equal scores at the k-th place is taken is unspecified), in
+    decreasing order of score, equal scores by lowest index.  zd_bits
+    [B, N, V]; returns int32 [B, N]."""
+    zd = f32_from_bf16_bits(zd_bits)
+    B, N = zd.shape[0], len(parent)
+    x = np.zeros((B, N), dtype=np.int32)
+    for p in range(-1, N):
+        kids = [n for n in range(N) if parent[n] == p]
+        if not kids:
+            continue
+        row = zd[:, p + 1]
+        k = len(kids)
+        top = np.argpartition(-row, k - 1, axis=-1)[:, :k] if k < row.shape[-1] else \
+            np.broadcast_to(np.arange(row.shape[-1]), row.shape)[:, :k]
+        # the k selected tokens by decreasing score, ties by lowest index
+        val = np.take_along_axis(row, top, axis=-1)
+        order = np.lexsort((top, -val), axis=-1)
+        x[:, kids] = np.take_along_axis(top, order, axis=-1)
+    return x
