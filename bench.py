@@ -224,6 +224,55 @@ def lm_head_parts(torch, p, wl, reps=12):
     return res
 
 
+def tree_parts(torch, p, wl, reps=12):
+    """Token-tree verification of B = 64 sequences, each a 25-node draft tree
+    (the EAGLE-style shape workloads.TREE25) over V = 128256: target logits
+    [64, 26, V] from a seeded device generator (a shared low-rank part plus
+    noise, like the chain workload), candidates the top-k of a correlated
+    draft row per parent.  Greedy and sampling (T = 0.7) timed like
+    time_parts.  Returns mean us and GB/s over the logits read once."""
+    cfg4 = wl.CONFIGS["C4"]
+    B, V, T = cfg4["B"], cfg4["V"], cfg4["temperature"]
+    par = torch.tensor(wl.TREE25, dtype=torch.int32)
+    N = par.numel()
+    g = torch.Generator(device="cuda")
+    g.manual_seed(777)
+    S = torch.randn((B, N + 1, 8), generator=g, device="cuda") @ torch.randn((8, V), generator=g, device="cuda")
+    S = S / 8 ** 0.5
+    zt = (3.0 * (0.98 * S + 0.2 * torch.randn((B, N + 1, V), generator=g, device="cuda"))).to(torch.bfloat16)
+    zd = 3.0 * (0.98 * S + 0.2 * torch.randn((B, N + 1, V), generator=g, device="cuda"))
+    del S
+    x = torch.empty((B, N), dtype=torch.int32, device="cuda")
+    for pnode in range(-1, N):
+        kids = [n for n in range(N) if int(par[n]) == pnode]
+        if kids:
+            x[:, kids] = torch.topk(zd[:, pnode + 1], len(kids), dim=-1).indices.to(torch.int32)
+    del zd
+    parents = par.to("cuda").repeat(B, 1).contiguous()
+    u = torch.rand((B, N + 1), generator=g, device="cuda")
+    ws = torch.empty((p.accept_tree_workspace_bytes(B, N, V),), dtype=torch.uint8, device="cuda")
+    out = torch.empty((B, N + 1), dtype=torch.int32, device="cuda")
+    nodes = torch.empty((B, N), dtype=torch.int32, device="cuda")
+    num = torch.empty((B,), dtype=torch.int32, device="cuda")
+    res = {}
+    for name, temp in (("greedy", 0.0), ("sampling", T)):
+        evs = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            p.verify_accept_tree(zt, parents, x, u if temp > 0 else None, temp, workspace=ws, out_tokens=out,
+                                 accepted_nodes=nodes, num_accepted=num)
+            e1.record()
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        us = float(np.mean([a.elapsed_time(b) for a, b in evs[2:]])) * 1e3
+        res[name + "_us"] = round(us, 1)
+        res[name + "_gbps"] = round(2.0 * B * (N + 1) * V / (us * 1e-6) / 1e9, 1)
+        res[name + "_mean_accepted_plus_one"] = round(float(num.float().mean().item()) + 1.0, 3)
+    res["workload"] = f"token-tree verification B={B}, 25-node tree, V={V}, bf16 target logits [B,26,V]"
+    return res
+
+
 def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40):
     """The oracle on the host cores, on a bounded sample of the benched step:
     the 4 linears at M=320 restricted to every `nfrac`-th output channel
@@ -395,6 +444,8 @@ def main(argv=None):
     parts, spread = time_parts(torch, step, weights, logits, reps=22)
     vendor = vendor_gemm(torch, step, weights)
     lm = lm_head_parts(torch, p, wl)
+    tree = tree_parts(torch, p, wl)
+    log(f"tree verification: greedy {tree['greedy_us']} us, sampling {tree['sampling_us']} us")
     log(f"LM head: gemm {lm['gemm']} us (with statistics {lm['gemm_with_stats']}); accept {lm['accept']} us "
         f"(from statistics {lm['accept_from_stats']}); unfused {lm['unfused_us']} us, fused {lm['fused_us']} us")
     gemm_us = parts["qkv"] + parts["o"] + parts["gate_up"] + parts["down"]
@@ -428,6 +479,7 @@ def main(argv=None):
             "hipblaslt_gemm_us": vendor,
             "part_us_p10_p90": spread,
             "lm_head_and_accept_us": lm,
+            "tree_accept": tree,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),
