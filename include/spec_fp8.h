@@ -146,6 +146,31 @@ spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, s
                           void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * spec_fp8_gemm_silu_mul -- the gated FFN's fused gate|up projection with the
+ * SiLU gate in its epilogue (the Llama-family target's FFN, section 4), so
+ * that the [M, 2I] gate|up output is never written:
+ *
+ *   yg = bf16_RNE(fl32(fl32(acc[m,c] * sa(m)) * sw(c)))           gate, weight row c
+ *   yu = bf16_RNE(fl32(fl32(acc[m,I+c] * sa(m)) * sw(I+c)))       up, weight row I + c
+ *   h[m,c] = bf16(silu(yg) * yu)                                  c < I
+ *
+ * i.e. spec_silu_mul_bf16 applied to spec_fp8_gemm's bf16 output (same device
+ * code for the gate), except that K is never split here and the fp32
+ * summation order of the accumulators may differ.  h is the input of the
+ * down projection's per-token quantize (spec_fp8_quantize, SPEC_QIN_BF16).
+ *
+ * W       uint8 E4M3 [2I, ldw]: rows 0..I-1 gate, I..2I-1 up (the layout the
+ *         SILU_MUL quantize input expects); w_scale [2I] or [1].
+ * a, lda, a_scale, a_mode, K: as spec_fp8_gemm.
+ * h       bf16 [M, ldh], I <= ldh, ldh % 8 == 0, 16-byte aligned.
+ * Requirements: I > 0 (SPEC_ERR_SHAPE), I % 8 == 0 (SPEC_ERR_UNSUPPORTED); the
+ * operand requirements of spec_fp8_gemm with N = 2I.  No workspace.
+ */
+spec_status spec_fp8_gemm_silu_mul(const uint8_t* a, int64_t lda, const float* a_scale, spec_scale_mode a_mode,
+                                   const uint8_t* w, int64_t ldw, const float* w_scale, spec_scale_mode w_mode,
+                                   int64_t M, int64_t I, int64_t K, void* h, int64_t ldh, void* stream);
+
+/*
  * spec_fp8_gemm_logit_stats -- the LM-head projection of the verify pass (the
  * target model's output layer over the M = B*(k+1) verify rows, hidden size K
  * to vocabulary V; section 3.1) as an FP8 GEMM whose epilogue also produces

@@ -18,6 +18,7 @@ from .ops import (  # noqa: F401
     gemm,
     gemm_workspace_bytes,
     gemm_logit_stats,
+    gemm_silu_mul,
     logit_stats_count,
     verify_accept,
     accept_workspace_bytes,

@@ -18,7 +18,7 @@ QIN_BF16, QIN_SILU_MUL_BF16 = 0, 1
 OUT_BF16, OUT_F32 = 0, 1
 
 EXPORTS = ("spec_fp8_quantize", "spec_silu_mul_bf16", "spec_fp8_gemm_workspace_bytes", "spec_fp8_gemm",
-           "spec_logit_stats_count", "spec_fp8_gemm_logit_stats",
+           "spec_fp8_gemm_silu_mul", "spec_logit_stats_count", "spec_fp8_gemm_logit_stats",
            "spec_verify_accept_workspace_bytes", "spec_verify_accept", "spec_verify_accept_stats",
            "spec_verify_accept_tree_workspace_bytes", "spec_verify_accept_tree",
            "spec_status_string", "spec_last_hip_error", "spec_version")
@@ -52,6 +52,8 @@ def load() -> ctypes.CDLL:
     lib.spec_fp8_gemm_workspace_bytes.restype = sz
     lib.spec_fp8_gemm.argtypes = [vp, i64, vp, i32, vp, i64, vp, i32, i64, i64, i64, vp, i64, i32, vp, sz, vp]
     lib.spec_fp8_gemm.restype = i32
+    lib.spec_fp8_gemm_silu_mul.argtypes = [vp, i64, vp, i32, vp, i64, vp, i32, i64, i64, i64, vp, i64, vp]
+    lib.spec_fp8_gemm_silu_mul.restype = i32
     lib.spec_logit_stats_count.argtypes = [i64, i64, i64]
     lib.spec_logit_stats_count.restype = sz
     lib.spec_fp8_gemm_logit_stats.argtypes = [vp, i64, vp, i32, vp, i64, vp, i32, i64, i64, i64, f32, vp, i64, vp,

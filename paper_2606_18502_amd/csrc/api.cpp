@@ -65,7 +65,7 @@ spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, s
 size_t spec_logit_stats_count(int64_t M, int64_t V, int64_t K) {
     if (M <= 0 || V <= 0 || K <= 0 || K % 128 != 0) return 0;
     if (M > 2147483647LL || V > 2147483647LL || K > 2147483647LL) return 0;
-    return (size_t)specfp8::plan_gemm(M, V, K, true).stat_groups;
+    return (size_t)specfp8::plan_gemm(M, V, K, specfp8::kEpiStats).stat_groups;
 }
 
 spec_status spec_fp8_gemm_logit_stats(const uint8_t* a, int64_t lda, const float* a_scale, spec_scale_mode a_mode,
@@ -75,7 +75,7 @@ spec_status spec_fp8_gemm_logit_stats(const uint8_t* a, int64_t lda, const float
     spec_status st = specfp8::check_gemm(a, lda, a_scale, (int)a_mode, w, ldw, w_scale, (int)w_mode, M, V, K, logits,
                                          ld_logits, SPEC_OUT_BF16);
     if (st != SPEC_OK) return st;
-    const specfp8::GemmPlan plan = specfp8::plan_gemm(M > 0 ? M : 1, V, K, true);
+    const specfp8::GemmPlan plan = specfp8::plan_gemm(M > 0 ? M : 1, V, K, specfp8::kEpiStats);
     st = specfp8::check_logit_stats(M, V, temperature, logits, ld_logits, stats, ld_stats, plan.stat_groups);
     if (st != SPEC_OK || M == 0) return st;
     const float c2 = temperature > 0.0f ? (float)(1.4426950408889634 / (double)temperature) : 0.0f;
@@ -83,6 +83,23 @@ spec_status spec_fp8_gemm_logit_stats(const uint8_t* a, int64_t lda, const float
                                          w_mode == SPEC_SCALE_PER_TENSOR, M, V, K, logits, ld_logits, 0, nullptr,
                                          as_stream(stream), temperature > 0.0f ? 1 : 2, c2,
                                          reinterpret_cast<float2*>(stats), ld_stats));
+}
+
+spec_status spec_fp8_gemm_silu_mul(const uint8_t* a, int64_t lda, const float* a_scale, spec_scale_mode a_mode,
+                                   const uint8_t* w, int64_t ldw, const float* w_scale, spec_scale_mode w_mode,
+                                   int64_t M, int64_t I, int64_t K, void* h, int64_t ldh, void* stream) {
+    if (I <= 0) return SPEC_ERR_SHAPE;
+    if (I % 8 != 0 || I > 1073741823LL) return SPEC_ERR_UNSUPPORTED;
+    if (ldh < I) return SPEC_ERR_SHAPE;
+    // the weight operand is [2I, K]; the output checks are those of a bf16 [M, I] result
+    spec_status st = specfp8::check_gemm(a, lda, a_scale, (int)a_mode, w, ldw, w_scale, (int)w_mode, M, 2 * I, K, h,
+                                         2 * I, SPEC_OUT_BF16);
+    if (st != SPEC_OK || M == 0) return st;
+    if (ldh % 8 != 0 || (reinterpret_cast<uintptr_t>(h) & 15u)) return SPEC_ERR_ALIGN;
+    const specfp8::GemmPlan plan = specfp8::plan_gemm(M, 2 * I, K, specfp8::kEpiSilu);
+    return from_hip(specfp8::launch_gemm(plan, a, lda, a_scale, a_mode == SPEC_SCALE_PER_TENSOR, w, ldw, w_scale,
+                                         w_mode == SPEC_SCALE_PER_TENSOR, M, 2 * I, K, h, ldh, 0, nullptr,
+                                         as_stream(stream), 0, 0.0f, nullptr, 0, I));
 }
 
 size_t spec_verify_accept_workspace_bytes(int64_t B, int64_t k, int64_t V) {
@@ -163,6 +180,6 @@ const char* spec_status_string(spec_status s) {
 
 int spec_last_hip_error(void) { return g_last_hip_error; }
 
-int spec_version(void) { return 300; }
+int spec_version(void) { return 400; }
 
 }  // extern "C"

@@ -21,6 +21,19 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
     return u >> 16;
 }
 
+// The SiLU gate of the FFN (shared by the SiLU-gated quantize and the GEMM
+// epilogue that fuses it, so both give the same h for the same g, u):
+// h = bf16(silu(g) * u) with silu(g) = g / (1 + e^-g) = g * rcp(1 + 2^(-g log2 e)),
+// in fp32 on the hardware exp2 and reciprocal (about 1 ulp each): the bf16
+// rounding of h only differs from an exact evaluation at near-ties.  Large
+// |g| saturate correctly: 2^(+big) = inf gives rcp = 0 (silu -> -0), and
+// 2^(-big) = 0 gives silu = g.
+__device__ __forceinline__ float silu_mul_bf16(float g, float u) {
+    const float e = __builtin_amdgcn_exp2f(g * -1.44269504088896341f);
+    const float sg = g * __builtin_amdgcn_rcpf(1.0f + e);
+    return bf16_to_f32(f32_to_bf16_rne(sg * u));
+}
+
 // Unpack 8 bf16 values held in a 16-byte vector.
 __device__ __forceinline__ void unpack8(const uint4& v, float out[8]) {
     out[0] = __uint_as_float(v.x << 16);

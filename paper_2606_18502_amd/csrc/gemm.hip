@@ -63,7 +63,18 @@ struct GemmArgs {
     int m_tiles, n_tiles, splits, ksteps;
     int stats_mode;   // 0: none; 1: (max t, sum 2^(t - max)), t = z * c2; 2: (max z, lowest column)
     float c2;
+    int silu_inter;   // > 0: SiLU-gated output of I = silu_inter columns from W = [gate; up] (N = 2I)
 };
+
+// Weight row of logical output column n.  With the SiLU-gated epilogue every
+// 16-row block of the weight tile pairs 8 gate rows with the matching 8 up
+// rows (logical block b holds gate c, up c for c = 8b .. 8b+7), so that one
+// lane exchange brings each h column's gate and up accumulators together.
+__device__ __forceinline__ int w_row(const GemmArgs& g, int n) {
+    if (g.silu_inter == 0) return n;
+    const int c = (n >> 4) * 8 + (n & 7);
+    return (n & 8) ? g.silu_inter + c : c;
+}
 
 __device__ __forceinline__ int xcd_remap(int b, int total) {
     // Blocks are dealt to XCDs round-robin (block b -> XCD b % 8).  Give each
@@ -112,7 +123,7 @@ __device__ __forceinline__ void issue_group(const GemmArgs& g, char* stage, int 
         src = g.a + (int64_t)m * g.lda + kbyte + chunk * 16;
     } else {
         int n = n0 + row - C::BM;
-        n = n < g.N ? n : g.N - 1;
+        n = w_row(g, n < g.N ? n : g.N - 1);
         src = g.w + (int64_t)n * g.ldw + kbyte + chunk * 16;
     }
     __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(stage + grp * 1024), 16, 0, 0);
@@ -275,7 +286,7 @@ __device__ __forceinline__ void load_scales(const GemmArgs& g, float (&sa_reg)[W
     for (int i = 0; i < WTN; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int n = min(n0 + (wn * WTN + i) * 16 + 4 * kg0 + r, g.N - 1);
+            const int n = w_row(g, min(n0 + (wn * WTN + i) * 16 + 4 * kg0 + r, g.N - 1));
             sw_reg[i][r] = g.w_per_tensor ? g.sw[0] : g.sw[n];
         }
 }
@@ -359,6 +370,27 @@ __device__ __forceinline__ void store_blocks(const GemmArgs& g, const v4f (&acc)
             uint32_t bits[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) bits[r] = f32_to_bf16_rne((acc[i][j][r] * sa_reg[j]) * sw_reg[i][r]);
+            if constexpr (STATS == 3) {
+                // lanes 16 kg + r16 with kg < 2 hold the gate of h columns
+                // (n - n0') / 2 + 4 kg + r (n0' = the block's first logical
+                // column), lanes with kg >= 2 the matching up values
+                float h[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float y = bf16_to_f32(bits[r]);
+                    const float other = __shfl_xor(y, 32, 64);
+                    h[r] = silu_mul_bf16(y, other);
+                }
+                const int hc = (n0 + (wn * WTN + i) * 16) / 2 + 4 * kg;    // first h column of this lane
+                if (kg < 2 && (!EDGE || (m < g.M && hc < g.silu_inter))) {
+                    uint16_t* hrow = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy;
+                    uint2 o;
+                    o.x = (__float_as_uint(h[0]) >> 16) | (__float_as_uint(h[1]) & 0xffff0000u);
+                    o.y = (__float_as_uint(h[2]) >> 16) | (__float_as_uint(h[3]) & 0xffff0000u);
+                    *reinterpret_cast<uint2*>(hrow + hc) = o;
+                }
+                continue;
+            }
             if constexpr (STATS == 1) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -395,7 +427,13 @@ __device__ __forceinline__ void store_blocks(const GemmArgs& g, const v4f (&acc)
 // K split the fp32 partial goes to the workspace instead.  Tiles wholly
 // inside the output take the unchecked path.
 //
-// STATS (bf16 output, no K split): the statistics of the stored values of
+// STATS 3 (SiLU-gated output, no K split): the tile's weight rows pair gate
+// and up rows (w_row), and each lane pair kg, kg ^ 2 of a block exchanges its
+// bf16-rounded values, so lanes kg < 2 store h = bf16(silu(gate) * up) for 4
+// consecutive h columns: exactly what the bf16 output followed by the
+// SiLU-gated quantize's input step gives for the same accumulators.
+//
+// STATS 1, 2 (bf16 output, no K split): the statistics of the stored values of
 // each row over the columns this wave holds (column group nt * WN + wn), for
 // the acceptance test of the logits: STATS 1 keeps (max t, sum 2^(t - max))
 // of t = fl32(z * c2) online while the row's values are stored; STATS 2 keeps
@@ -416,7 +454,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[W
         store_blocks<WTM, WTN, STATS, false>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, sm, ss);
     else
         store_blocks<WTM, WTN, STATS, true>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, sm, ss);
-    if constexpr (STATS != 0) {
+    if constexpr (STATS == 1 || STATS == 2) {
         const int kg = lane >> 4;
         const int r16 = lane & 15;
         const int64_t col = (int64_t)nt * WN + wn;
@@ -600,6 +638,11 @@ constexpr int kCfgWN[kKinds] = {2, 2, 2, 2, 2, 2, 1, 2, 2};   // waves across N 
 template <class C, int WTM, int WTN, int WM, int WN, int STAGES, bool WITH_STATS = true>
 hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
     const int total = g.m_tiles * g.n_tiles * g.splits;
+    if (g.silu_inter > 0) {
+        hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 3>), dim3(total), dim3(C::kThreads), 0,
+                           stream, g);
+        return hipGetLastError();
+    }
     if constexpr (WITH_STATS) {
         if (g.stats_mode == 1) {
             hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 1>), dim3(total), dim3(C::kThreads), 0,
@@ -619,8 +662,9 @@ hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
 
 }  // namespace
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool no_split) {
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     GemmPlan p{};
+    const bool no_split = epilogue != kEpiPlain;
     // Tile shapes by measurement on MI355X (M = B*(k+1) verify rows):
     //   M <= 64: 64x64;  M <= 80: 80x128;
     //   M <= 320: 160x224 when N fills >= 64 such columns exactly (gate|up),
@@ -640,7 +684,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool no_split) {
     else p.kind = 2;
     // with the statistics epilogue the 160x224 tile would spill registers;
     // 160x192 (ragged last tile where N % 192 != 0) takes its place
-    if (no_split && p.kind == 2) p.kind = 4;
+    if (epilogue == kEpiStats && p.kind == 2) p.kind = 4;
     const int ksteps = (int)(K / kBK);
     int splits = 0;
 #ifdef SPECFP8_TUNING
@@ -679,9 +723,11 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool no_split) {
 hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const float* sa, int a_per_tensor,
                        const uint8_t* w, int64_t ldw, const float* sw, int w_per_tensor, int64_t M,
                        int64_t N, int64_t K, void* y, int64_t ldy, int out_f32, void* workspace,
-                       hipStream_t stream, int stats_mode, float c2, float2* stats, int64_t ld_stats) {
+                       hipStream_t stream, int stats_mode, float c2, float2* stats, int64_t ld_stats,
+                       int64_t silu_inter) {
     GemmArgs g;
     g.stats = stats; g.ld_stats = ld_stats; g.stats_mode = stats_mode; g.c2 = c2;
+    g.silu_inter = (int)silu_inter;
     g.a = a; g.w = w; g.sa = sa; g.sw = sw; g.y = y;
     g.partial = reinterpret_cast<float*>(workspace);
     g.lda = lda; g.ldw = ldw; g.ldy = ldy; g.ldp = p.ldp;

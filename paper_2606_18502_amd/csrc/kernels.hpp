@@ -22,8 +22,10 @@ struct GemmPlan {
     int64_t ldp;           // row stride of the fp32 partial tiles
     size_t workspace_bytes;
 };
-// no_split: one workgroup per output tile (required for epilogue statistics)
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool no_split = false);
+// Epilogue of a plan: plain (K may be split), logit statistics, or the
+// SiLU-gated output; the last two keep one workgroup per output tile.
+enum GemmEpilogue { kEpiPlain = 0, kEpiStats = 1, kEpiSilu = 2 };
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue = kEpiPlain);
 // stats_mode 0: plain GEMM; 1/2: also the per-(row, column group) statistics
 // of the bf16 output (softmax in base 2 with c2 = log2(e)/T, or argmax) into
 // stats [M][ld_stats]; requires p.splits == 1.
@@ -31,7 +33,9 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
                        const uint8_t* w, int64_t ldw, const float* sw, int w_per_tensor, int64_t M,
                        int64_t N, int64_t K, void* y, int64_t ldy, int out_f32, void* workspace,
                        hipStream_t stream, int stats_mode = 0, float c2 = 0.0f, float2* stats = nullptr,
-                       int64_t ld_stats = 0);
+                       int64_t ld_stats = 0, int64_t silu_inter = 0);
+// SiLU-gated output: N = 2I weight rows [gate; up], y = h [M, ldy] bf16 with
+// I = silu_inter columns; the plan comes from plan_gemm(M, 2I, K, kEpiSilu).
 
 // ---- accept.hip
 struct AcceptPlan {

@@ -19,17 +19,6 @@ namespace {
 constexpr int kQThreads = 256;       // threads of the element-wise kernel
 constexpr int kQMaxThreads = 1024;   // threads per row of the row kernel, at most
 
-// h = bf16(silu(g) * u) with silu(g) = g / (1 + e^-g) = g * rcp(1 + 2^(-g log2 e)),
-// in fp32 on the hardware exp2 and reciprocal (about 1 ulp each): the bf16
-// rounding of h only differs from an exact evaluation at near-ties.  Large
-// |g| saturate correctly: 2^(+big) = inf gives rcp = 0 (silu -> -0), and
-// 2^(-big) = 0 gives silu = g.
-__device__ __forceinline__ float silu_mul_bf16(float g, float u) {
-    const float e = __builtin_amdgcn_exp2f(g * -1.44269504088896341f);
-    const float sg = g * __builtin_amdgcn_rcpf(1.0f + e);
-    return bf16_to_f32(f32_to_bf16_rne(sg * u));
-}
-
 template <int IN_KIND>
 __device__ __forceinline__ void load_chunk(const uint16_t* __restrict__ xrow, int64_t cols,
                                            int64_t c, float v[8]) {

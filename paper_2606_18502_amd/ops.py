@@ -158,6 +158,33 @@ def _scale_modes(a, sa, w, sw):
     return a_mode, w_mode
 
 
+def gemm_silu_mul(a: torch.Tensor, sa: torch.Tensor, w: torch.Tensor, sw: torch.Tensor,
+                  out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """h = bf16(silu(gate) * up) of the fused gate|up projection (spec_fp8_gemm_silu_mul).
+
+    a: uint8 E4M3 [M,K]; w: uint8 E4M3 [2I,K] (gate rows, then up rows);
+    sa, sw as for gemm.  Returns h bf16 [M,I].
+    """
+    lib = _lib.load()
+    _dev(a, torch.uint8, "a")
+    _dev(w, torch.uint8, "w")
+    _dev(sa, torch.float32, "sa")
+    _dev(sw, torch.float32, "sw")
+    M, K = a.shape
+    if w.shape[1] != K or w.shape[0] % 2:
+        raise ValueError("w must be [2I, K] with the activations' K")
+    I = w.shape[0] // 2
+    a_mode, w_mode = _scale_modes(a, sa, w, sw)
+    if out is None:
+        ld = (I + 7) // 8 * 8
+        out = torch.empty((M, ld), dtype=torch.bfloat16, device=a.device)[:, :I]
+    _dev(out, torch.bfloat16, "out")
+    check("spec_fp8_gemm_silu_mul", lib.spec_fp8_gemm_silu_mul(
+        a.data_ptr(), _rowmajor(a, "a"), sa.data_ptr(), a_mode, w.data_ptr(), _rowmajor(w, "w"), sw.data_ptr(),
+        w_mode, M, I, K, out.data_ptr(), _rowmajor(out, "out"), _stream()))
+    return out
+
+
 def logit_stats_count(M: int, V: int, K: int) -> int:
     return int(_lib.load().spec_logit_stats_count(M, V, K))
 

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.spec_version() == 300
+    assert lib.spec_version() == 400
     for s in range(9):
         assert lib.spec_status_string(s)
     assert lib.spec_status_string(99) == b"unknown status"
@@ -229,3 +229,20 @@ def test_accept_tree_validation(lib):
     assert tr(lib, wsb=need - 1) == WS
     assert tr(lib, ws=A16 + 8, wsb=need) == ALIGN
     assert tr(lib, B=0, zt=None, par=None, tok=None, u=None, out=None, nodes=None, num=None, ws=None, wsb=0) == OK
+
+
+def gs(lib, a=A16, lda=512, sa=A16, am=0, w=A16, ldw=512, sw=A16, wm=0, M=8, I=512, K=512, h=A16, ldh=512):
+    return lib.spec_fp8_gemm_silu_mul(a, lda, sa, am, w, ldw, sw, wm, M, I, K, h, ldh, None)
+
+
+def test_gemm_silu_mul_validation(lib):
+    assert gs(lib, I=0) == SHAPE
+    assert gs(lib, I=36, ldh=40) == UNSUP           # I % 8
+    assert gs(lib, ldh=256) == SHAPE                # ldh < I
+    assert gs(lib, am=2) == ENUM
+    assert gs(lib, K=500) == UNSUP
+    assert gs(lib, a=None) == NULL
+    assert gs(lib, h=None) == NULL
+    assert gs(lib, h=A1) == ALIGN
+    assert gs(lib, ldh=516) == ALIGN
+    assert gs(lib, M=0, a=None, sa=None, w=None, sw=None, h=None) == OK
