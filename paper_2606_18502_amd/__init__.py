@@ -6,6 +6,11 @@ W8A8 -- dynamic per-token activation quantization, per-output-channel weight
 scales, an fp32-accumulated FP8-MFMA GEMM with a scale epilogue -- followed by
 greedy or speculative-sampling acceptance of the drafted tokens.
 
+Beside the chain verify step it offers the LM-head GEMM with the acceptance
+statistics in its epilogue (gemm_logit_stats, then verify_accept with
+target_stats), the gate|up GEMM with the SiLU gate in its epilogue
+(gemm_silu_mul) and token-tree verification (verify_accept_tree).
+
 The computation lives in libspecfp8.so (HIP kernels behind the C ABI of
 include/spec_fp8.h); this package only marshals torch tensors into that ABI.
 """

@@ -15,6 +15,14 @@
 //                          chunk holding u*R, scans it in vocabulary order and
 //                          writes the tokens.
 //
+// Two variants reuse these kernels:
+//   target statistics given (the LM head's epilogue wrote them): the streaming
+//     kernel reads only the draft rows, and the merges read the given entries
+//     for the target rows (clear_tickets_kernel when nothing is streamed);
+//   token trees: the streaming kernels run over the N+1 target rows of every
+//     sequence, then tree_greedy_kernel / tree_sample_kernel walk the tree
+//     (see the token-tree section below).
+//
 // The two streaming kernels run a persistent grid in which every WAVE walks
 // (row, slice) items of 4096 logits with the loads of its next item in flight
 // while it reduces the current one, so HBM sees one continuous stream of

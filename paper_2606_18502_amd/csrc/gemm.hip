@@ -14,10 +14,10 @@
 //    global memory straight into LDS with global_load_lds_dwordx4 (no VGPR
 //    staging): one wave instruction moves 8 rows x 128 bytes = 1 KiB;
 //  * inside LDS each 128-byte row holds its eight 16-byte chunks in XOR-
-//    swizzled slots (slot = chunk ^ (row & 7)); the swizzle is applied on the
-//    global side, so global reads stay fully coalesced, and the MFMA operand
-//    reads (ds_read_b128, 8 lanes on 8 different rows, same logical chunk)
-//    hit 8 distinct slots -- no bank conflicts;
+//    swizzled slots (slot = chunk ^ ((row >> 1) & 7), see swz); the swizzle is
+//    applied on the global side, so global reads stay fully coalesced, and the
+//    MFMA operand reads (ds_read_b128 of one logical chunk from 16
+//    consecutive rows) hit 16 distinct 16-byte bank groups -- no conflicts;
 //  * STAGES buffers rotate so that STAGES-1 K-steps of loads are in flight
 //    while the current one is multiplied.
 //
@@ -27,6 +27,14 @@
 // Workgroup ids are remapped so that the tiles and K-splits that share
 // operands run on the same XCD (blocks are dealt round-robin to the 8 XCDs),
 // which keeps re-read operand bytes in that XCD's L2.
+//
+// Epilogue variants (a template argument, so each is its own kernel):
+//  0  the scaled output, bf16 or fp32, or the split-K partials;
+//  1  bf16 logits plus per-row softmax statistics of the stored values over
+//     each wave's columns (the LM head of the verify pass);
+//  2  bf16 logits plus per-row (max, lowest column) over each wave's columns;
+//  3  the SiLU-gated FFN output h = bf16(silu(gate) * up) from a weight tile
+//     whose 16-row blocks pair 8 gate rows with the matching 8 up rows.
 #include <float.h>
 
 #include "device_common.hpp"
