@@ -93,3 +93,86 @@ def test_graph_replays_match_eager():
         # eager work between replays on the same buffers
         p.gemm(q1, s1, w1q, w1s, out=y1, workspace=gws)
         torch.cuda.synchronize()
+
+
+def test_graph_replays_of_the_lm_head_and_tree_paths():
+    """The LM head with statistics followed by the acceptance from those
+    statistics, and the token-tree acceptance (greedy and sampling), captured
+    once and replayed with new inputs: every replay equals eager launches, and
+    two eager runs agree (determinism)."""
+    p = need_gpu()
+    dev = "cuda"
+    B, k, K, V, T = 6, 3, 512, 3000, 0.8
+    M = B * (k + 1)
+    N = 9
+    par = torch.tensor([-1, -1, 0, 0, 1, 2, 2, 4, 5], dtype=torch.int32, device=dev).repeat(B, 1).contiguous()
+    hq = torch.empty((M, K), dtype=torch.uint8, device=dev)
+    hs = torch.empty((M,), dtype=torch.float32, device=dev)
+    wq = torch.empty((V, K), dtype=torch.uint8, device=dev)
+    wsc = torch.empty((V,), dtype=torch.float32, device=dev)
+    zd = torch.empty((B, k, V), dtype=torch.bfloat16, device=dev)
+    xt = torch.empty((B, k), dtype=torch.int32, device=dev)
+    u = torch.empty((B, k + 1), dtype=torch.float32, device=dev)
+    zt_tree = torch.empty((B, N + 1, V), dtype=torch.bfloat16, device=dev)
+    x_tree = torch.empty((B, N), dtype=torch.int32, device=dev)
+    u_tree = torch.empty((B, N + 1), dtype=torch.float32, device=dev)
+    logits = torch.empty((M, V), dtype=torch.bfloat16, device=dev)
+    stats = torch.empty((M, p.logit_stats_count(M, V, K), 2), dtype=torch.float32, device=dev)
+    aws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device=dev)
+    tws = torch.empty((p.accept_tree_workspace_bytes(B, N, V),), dtype=torch.uint8, device=dev)
+    outs = [torch.empty((B, k + 1), dtype=torch.int32, device=dev), torch.empty((B,), dtype=torch.int32, device=dev),
+            torch.empty((B, N + 1), dtype=torch.int32, device=dev), torch.empty((B, N), dtype=torch.int32, device=dev),
+            torch.empty((B,), dtype=torch.int32, device=dev), torch.empty((B, N + 1), dtype=torch.int32, device=dev),
+            torch.empty((B, N), dtype=torch.int32, device=dev), torch.empty((B,), dtype=torch.int32, device=dev)]
+
+    def load(seed):
+        a, s = p.quantize(dev_bf16(wl.linear_activations(M, K, seed, 0.01, 20.0)))
+        hq.copy_(a); hs.copy_(s)
+        a, s = p.quantize(dev_bf16(wl.linear_weights(V, K, seed + 1, 0.1)))
+        wq.copy_(a); wsc.copy_(s)
+        _, d_ = wl.accept_logits(B, k, V, seed + 2, 0.8)
+        zd.copy_(dev_bf16(d_))
+        xt.copy_(dev_i32(wl.draft_tokens_sampled(d_, T, seed=seed + 3)))
+        u.copy_(dev_f32(wl.philox_uniforms((B, k + 1), seed=seed + 4)))
+        t_, dd = wl.accept_logits(B, N, V, seed + 5, 0.95)
+        zt_tree.copy_(dev_bf16(t_))
+        x_tree.copy_(dev_i32(wl.tree_tokens_topk(dd, par[0].cpu().numpy())))
+        u_tree.copy_(dev_f32(wl.philox_uniforms((B, N + 1), seed=seed + 6)))
+
+    def step():
+        p.gemm_logit_stats(hq, hs, wq, wsc, T, out=logits, stats=stats)
+        p.verify_accept(logits.view(B, k + 1, V), zd, xt, u, T, workspace=aws, out_tokens=outs[0],
+                        num_accepted=outs[1], target_stats=stats)
+        p.verify_accept_tree(zt_tree, par, x_tree, None, 0.0, workspace=tws, out_tokens=outs[2],
+                             accepted_nodes=outs[3], num_accepted=outs[4])
+        p.verify_accept_tree(zt_tree, par, x_tree, u_tree, T, workspace=tws, out_tokens=outs[5],
+                             accepted_nodes=outs[6], num_accepted=outs[7])
+
+    def snapshot():
+        torch.cuda.synchronize()
+        return [t.detach().clone() for t in [logits, stats] + outs]
+
+    load(10)
+    step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    for rep, seed in enumerate((20, 30, 30)):
+        say(f"graph replay {rep} (inputs seed {seed})")
+        load(seed)
+        step()
+        ref = snapshot()
+        step()
+        again = snapshot()
+        for a, b in zip(again, ref):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), rep     # deterministic
+        for t in outs:
+            t.fill_(-7)
+        stats.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        got = snapshot()
+        for i, (a, b) in enumerate(zip(got, ref)):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), (rep, i)
