@@ -306,8 +306,9 @@ spec_status spec_verify_accept_stats(const void* target_logits, const float* tar
  * num_accepted   int32 [B]: path length a_b; a_b + 1 tokens are emitted.
  * workspace      >= spec_verify_accept_tree_workspace_bytes(B, N, V); contents on entry
  *                are ignored.
- * Requirements: B >= 0 (0 is a no-op), 1 <= N <= 64, 1 <= V <= 2^22, B <= 65535
- * (SPEC_ERR_UNSUPPORTED otherwise); temperature finite and >= 0 (SPEC_ERR_VALUE).
+ * Requirements: B >= 0 (0 is a no-op), 1 <= N <= 64, 1 <= V <= 2^22, B <= 65535,
+ * B*(N+1)*ceil(V/4096) < 2^31 (SPEC_ERR_UNSUPPORTED otherwise); temperature finite
+ * and >= 0 (SPEC_ERR_VALUE).
  * Probabilities are computed in fp32 (the accept tests in double from fp32
  * statistics); a decision within ~1e-5 relative of its boundary may differ from
  * an exact evaluation.

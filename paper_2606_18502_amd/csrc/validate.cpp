@@ -92,6 +92,8 @@ spec_status check_accept_tree(const void* target_logits, const int32_t* parents,
     if (!isfinite(temperature) || temperature < 0.0f) return SPEC_ERR_VALUE;
     if (B < 0 || N < 1 || V < 1) return SPEC_ERR_SHAPE;
     if (N > 64 || V > 4194304LL || B > kMaxGridY) return SPEC_ERR_UNSUPPORTED;
+    // the streaming kernels count (row, 4096-logit slice) items in 31 bits
+    if (B * (N + 1) * ((V + 4095) / 4096) > 2147483647LL) return SPEC_ERR_UNSUPPORTED;
     if (B == 0) return SPEC_OK;
     if (!target_logits || !parents || !tokens || !out_tokens || !accepted_nodes || !num_accepted)
         return SPEC_ERR_NULL;

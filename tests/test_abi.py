@@ -217,6 +217,8 @@ def test_accept_tree_validation(lib):
     assert tr(lib, N=65) == UNSUP
     assert tr(lib, V=(1 << 22) + 8) == UNSUP
     assert tr(lib, B=70000) == UNSUP
+    assert tr(lib, B=65535, N=64, V=1 << 22) == UNSUP      # more than 2^31 streaming items
+    assert tr(lib, B=1000, N=64, V=1 << 22, ws=None) == WS   # within the item limit
     assert tr(lib, par=None) == NULL
     assert tr(lib, tok=None) == NULL
     assert tr(lib, nodes=None) == NULL
