@@ -19,6 +19,11 @@ inline spec_status from_hip(hipError_t e) {
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// One workgroup per (tile, K-split): the grid is an int.
+inline bool grid_fits(const specfp8::GemmPlan& p) {
+    return (int64_t)p.m_tiles * p.n_tiles * p.splits <= 2147483647LL;
+}
+
 }  // namespace
 
 extern "C" {
@@ -53,6 +58,7 @@ spec_status spec_fp8_gemm(const uint8_t* a, int64_t lda, const float* a_scale, s
                                                y, ldy, (int)out_dtype);
     if (st != SPEC_OK || M == 0) return st;
     const specfp8::GemmPlan plan = specfp8::plan_gemm(M, N, K);
+    if (!grid_fits(plan)) return SPEC_ERR_UNSUPPORTED;
     if (plan.workspace_bytes > 0) {
         if (!workspace || workspace_bytes < plan.workspace_bytes) return SPEC_ERR_WORKSPACE;
         if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return SPEC_ERR_ALIGN;
@@ -78,6 +84,7 @@ spec_status spec_fp8_gemm_logit_stats(const uint8_t* a, int64_t lda, const float
     const specfp8::GemmPlan plan = specfp8::plan_gemm(M > 0 ? M : 1, V, K, specfp8::kEpiStats);
     st = specfp8::check_logit_stats(M, V, temperature, logits, ld_logits, stats, ld_stats, plan.stat_groups);
     if (st != SPEC_OK || M == 0) return st;
+    if (!grid_fits(plan)) return SPEC_ERR_UNSUPPORTED;
     const float c2 = temperature > 0.0f ? (float)(1.4426950408889634 / (double)temperature) : 0.0f;
     return from_hip(specfp8::launch_gemm(plan, a, lda, a_scale, a_mode == SPEC_SCALE_PER_TENSOR, w, ldw, w_scale,
                                          w_mode == SPEC_SCALE_PER_TENSOR, M, V, K, logits, ld_logits, 0, nullptr,
@@ -97,6 +104,7 @@ spec_status spec_fp8_gemm_silu_mul(const uint8_t* a, int64_t lda, const float* a
     if (st != SPEC_OK || M == 0) return st;
     if (ldh % 8 != 0 || (reinterpret_cast<uintptr_t>(h) & 15u)) return SPEC_ERR_ALIGN;
     const specfp8::GemmPlan plan = specfp8::plan_gemm(M, 2 * I, K, specfp8::kEpiSilu);
+    if (!grid_fits(plan)) return SPEC_ERR_UNSUPPORTED;
     return from_hip(specfp8::launch_gemm(plan, a, lda, a_scale, a_mode == SPEC_SCALE_PER_TENSOR, w, ldw, w_scale,
                                          w_mode == SPEC_SCALE_PER_TENSOR, M, 2 * I, K, h, ldh, 0, nullptr,
                                          as_stream(stream), 0, 0.0f, nullptr, 0, I));

@@ -705,7 +705,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     const int bm = kCfgBM[p.kind], bn = kCfgBN[p.kind];
     p.m_tiles = (int)((M + bm - 1) / bm);
     p.n_tiles = (int)((N + bn - 1) / bn);
-    const int tiles = p.m_tiles * p.n_tiles;
+    const int64_t tiles = (int64_t)p.m_tiles * p.n_tiles;
     if (no_split) splits = 1;
     if (splits <= 0) {
         // Split K only when at most half of the 256 compute units would get

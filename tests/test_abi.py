@@ -116,6 +116,9 @@ def test_gemm_validation(lib):
     assert g(lib, M=320, N=1024, K=4096, lda=4096, ldw=4096, ldy=1024, ws=A16, wsb=need - 1) == WS
     assert g(lib, M=320, N=1024, K=4096, lda=4096, ldw=4096, ldy=1024, ws=A1, wsb=need) == ALIGN
     assert lib.spec_fp8_gemm_workspace_bytes(8, 1024, 100) == 0
+    # more output tiles than an int grid holds
+    big = (1 << 31) - 1
+    assert g(lib, M=big, N=big, K=128, lda=128, ldw=128, ldy=big + 1) == UNSUP
 
 
 def acc(lib, zt=A16, zd=A16, x=A16, u=A16, B=2, k=3, V=256, T=0.7, out=A16, num=A16, ws=A16, wsb=1 << 20):
