@@ -18,4 +18,4 @@ bounds, integer-exact GEMMs, one-hot selections, exact Fraction enumeration of
 the speculative-sampling law, the closed-form expected acceptance length).
 """
 
-from . import e4m3, quantize, gemm, accept, enumerate  # noqa: F401
+from . import e4m3, quantize, gemm, accept, enumerate, kvcache  # noqa: F401

@@ -19,5 +19,6 @@ from .gen import (  # noqa: F401
     philox_uniforms,
     tree_shape,
     tree_tokens_topk,
+    paged_slot_mapping,
 )
 from .configs import CONFIGS, C4_CORRELATION, TREE25  # noqa: F401

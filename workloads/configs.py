@@ -61,6 +61,13 @@ CONFIGS = {
         B=64, k=4, V=VOCAB, logit_std=3.0, rank=8, temperature=0.7,
         seed=7, draft_seed=8, uniform_seed=7,
     ),
+    "KV": dict(
+        desc="FP8 KV-cache write of the verify step's new tokens: B=64, k=4 -> T=320 tokens, "
+             "8 KV heads of 128 (Llama 3.1 8B), paged cache with 16-token blocks, "
+             "contexts of 512..4096 tokens per sequence",
+        B=64, k=4, T=320, H=8, D=128, block_size=16, ctx_min=512, ctx_max=4096,
+        key_outlier_frac=0.01, key_outlier_scale=20.0, seed=11,
+    ),
     "C5": dict(
         desc="long-prompt prefill/calibration: M=4096, 4096->14336 and 14336->4096, "
              "Student-t(3) activations, static per-tensor vs dynamic per-token scales",

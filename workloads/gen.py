@@ -183,3 +183,25 @@ def tree_tokens_topk(zd_bits: np.ndarray, parent: np.ndarray) -> np.ndarray:
         order = np.lexsort((top, -val), axis=-1)
         x[:, kids] = np.take_along_axis(top, order, axis=-1)
     return x
+
+
+def paged_slot_mapping(B: int, new_tokens: int, ctx_lens, block_size: int, seed: int):
+    """Cache slots of the verify step's new tokens in a paged KV cache.
+
+    Sequence b already holds ctx_lens[b] tokens; its new_tokens tokens take
+    positions ctx_lens[b] .. ctx_lens[b] + new_tokens - 1.  Every sequence
+    owns ceil((ctx_lens[b] + new_tokens) / block_size) blocks, drawn as one
+    seeded random permutation of all blocks, and position p of sequence b
+    lives in slot page[b][p // block_size] * block_size + p % block_size.
+    Returns (slot_mapping int64 [B * new_tokens] in sequence-major token
+    order, num_slots)."""
+    ctx = np.asarray(ctx_lens, dtype=np.int64)
+    need = (ctx + new_tokens + block_size - 1) // block_size
+    perm = _rng(seed).permutation(int(need.sum()))
+    starts = np.concatenate([[0], np.cumsum(need)[:-1]])
+    slots = np.empty(B * new_tokens, dtype=np.int64)
+    for b in range(B):
+        page = perm[starts[b]:starts[b] + need[b]]
+        pos = ctx[b] + np.arange(new_tokens)
+        slots[b * new_tokens:(b + 1) * new_tokens] = page[pos // block_size] * block_size + pos % block_size
+    return slots, int(need.sum()) * block_size
