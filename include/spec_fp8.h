@@ -120,6 +120,45 @@ spec_status spec_silu_mul_bf16(const void* x, int64_t rows, int64_t cols, int64_
                                void* h, int64_t ld_h, void* stream);
 
 /*
+ * spec_fp8_kv_cache_write -- the verify step's new keys and values, quantized
+ * to E4M3 and stored in a paged FP8 KV cache.
+ *
+ * Section 3.2 (FP8 Post-Training Quantization) stores the KV cache in FP8,
+ * half the bytes of bf16.  For every new token t < T whose slot
+ * s = slot_mapping[t] lies in [0, num_slots), and every KV head h < H, the
+ * key row kx = k[t*ld_k + h*D ...] (D bf16 values) is encoded as
+ *
+ *   PER_ROW:    sk = max(fl32(max_d |kx[d]| / 448), 2^-100);  k_scale[s*H + h] = sk  (written)
+ *   PER_TENSOR: sk = k_scale[0]                                                    (read)
+ *   k_cache[(s*H + h)*D + d] = E4M3(fl32(kx[d] * fl32(1 / sk)))
+ *
+ * and the value rows likewise with v, v_scale and v_cache; the encoding is
+ * spec_fp8_quantize's, bit for bit.  A token whose slot is negative (padding)
+ * or >= num_slots is skipped: nothing of its rows is written.  Slots of
+ * different tokens must differ; if two tokens share a slot, which one's
+ * codes (and scales) end up there is unspecified.  The static per-tensor
+ * scales of the paper's min-max scheme come from spec_fp8_quantize with
+ * SPEC_SCALE_CALIBRATE over calibration keys (or values) viewed as [T, H*D].
+ *
+ * k, v       bf16 [T, ld_k] / [T, ld_v]; head h of a token at columns [h*D, (h+1)*D);
+ *            the K and V column blocks of the QKV projection's output fit directly.
+ * slot_mapping  int64 [T].
+ * k_scale, v_scale  fp32 [num_slots, H] (PER_ROW, written at the slots stored) or fp32 [1]
+ *            (PER_TENSOR, read; finite and > 0).
+ * k_cache, v_cache  uint8 [num_slots, H, D] codes: slot-major, so a paged cache of blocks
+ *            [num_blocks, block_size, H, D] is the same memory with slot =
+ *            block * block_size + offset.  Untouched slots keep their contents.
+ * Requirements: T >= 0 (0 is a no-op), H > 0, D > 0, num_slots >= 0, ld_k and ld_v >= H*D
+ * (SPEC_ERR_SHAPE); D % 8 == 0 and D <= 512 (SPEC_ERR_UNSUPPORTED); k, v, k_cache and
+ * v_cache 16-byte aligned, ld_k and ld_v multiples of 8, slot_mapping 8-byte and the scales
+ * 4-byte aligned (SPEC_ERR_ALIGN).  mode must be PER_ROW or PER_TENSOR (SPEC_ERR_ENUM).
+ */
+spec_status spec_fp8_kv_cache_write(const void* k, int64_t ld_k, const void* v, int64_t ld_v,
+                                    const int64_t* slot_mapping, int64_t T, int64_t H, int64_t D,
+                                    int64_t num_slots, spec_scale_mode mode, float* k_scale, float* v_scale,
+                                    uint8_t* k_cache, uint8_t* v_cache, void* stream);
+
+/*
  * spec_fp8_gemm -- the W8A8 linear layer (section 3.2):
  *
  *   acc[m,n] = sum_k dec(A[m,k]) * dec(W[n,k])     accumulated in fp32

@@ -9,7 +9,8 @@ greedy or speculative-sampling acceptance of the drafted tokens.
 Beside the chain verify step it offers the LM-head GEMM with the acceptance
 statistics in its epilogue (gemm_logit_stats, then verify_accept with
 target_stats), the gate|up GEMM with the SiLU gate in its epilogue
-(gemm_silu_mul) and token-tree verification (verify_accept_tree).
+(gemm_silu_mul), token-tree verification (verify_accept_tree) and the
+FP8 KV-cache write of the new tokens' keys and values (kv_cache_write).
 
 The computation lives in libspecfp8.so (HIP kernels behind the C ABI of
 include/spec_fp8.h); this package only marshals torch tensors into that ABI.
@@ -20,6 +21,7 @@ from .ops import (  # noqa: F401
     quantize,
     calibrate,
     silu_mul,
+    kv_cache_write,
     gemm,
     gemm_workspace_bytes,
     gemm_logit_stats,

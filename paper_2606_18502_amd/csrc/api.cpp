@@ -45,6 +45,19 @@ spec_status spec_silu_mul_bf16(const void* x, int64_t rows, int64_t cols, int64_
                                              reinterpret_cast<uint16_t*>(h), ld_h, as_stream(stream)));
 }
 
+spec_status spec_fp8_kv_cache_write(const void* k, int64_t ld_k, const void* v, int64_t ld_v,
+                                    const int64_t* slot_mapping, int64_t T, int64_t H, int64_t D,
+                                    int64_t num_slots, spec_scale_mode mode, float* k_scale, float* v_scale,
+                                    uint8_t* k_cache, uint8_t* v_cache, void* stream) {
+    const spec_status st = specfp8::check_kv_cache_write(k, ld_k, v, ld_v, slot_mapping, T, H, D, num_slots,
+                                                         (int)mode, k_scale, v_scale, k_cache, v_cache);
+    if (st != SPEC_OK || T == 0 || num_slots == 0) return st;
+    return from_hip(specfp8::launch_kv_cache_write(
+        reinterpret_cast<const uint16_t*>(k), ld_k, reinterpret_cast<const uint16_t*>(v), ld_v, slot_mapping, T, H,
+        D, num_slots, mode == SPEC_SCALE_PER_TENSOR ? 1 : 0, k_scale, v_scale, k_cache, v_cache,
+        as_stream(stream)));
+}
+
 size_t spec_fp8_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
     if (M <= 0 || N <= 0 || K <= 0 || K % 128 != 0) return 0;
     return specfp8::plan_gemm(M, N, K).workspace_bytes;
@@ -188,6 +201,6 @@ const char* spec_status_string(spec_status s) {
 
 int spec_last_hip_error(void) { return g_last_hip_error; }
 
-int spec_version(void) { return 400; }
+int spec_version(void) { return 410; }
 
 }  // extern "C"

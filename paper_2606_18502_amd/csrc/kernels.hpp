@@ -13,6 +13,15 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t cols, int64_
 hipError_t launch_silu_mul(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x,
                            uint16_t* h, int64_t ld_h, hipStream_t stream);
 
+// ---- kvcache.hip
+// Keys and values of T new tokens ([T][ld] bf16, H heads of D values each) to
+// E4M3 codes in the slot-major caches [num_slots][H][D]; per-row scales go to
+// [num_slots][H], a per-tensor scale is read from [0].
+hipError_t launch_kv_cache_write(const uint16_t* k, int64_t ld_k, const uint16_t* v, int64_t ld_v,
+                                 const int64_t* slot_mapping, int64_t T, int64_t H, int64_t D,
+                                 int64_t num_slots, int per_tensor, float* k_scale, float* v_scale,
+                                 uint8_t* k_cache, uint8_t* v_cache, hipStream_t stream);
+
 // ---- gemm.hip
 struct GemmPlan {
     int kind;              // tile configuration

@@ -1,6 +1,7 @@
 #include "validate.hpp"
 
 #include <math.h>
+#include <stdint.h>
 
 namespace specfp8 {
 
@@ -41,6 +42,28 @@ spec_status check_silu_mul(const void* x, int64_t rows, int64_t cols, int64_t ld
     if (rows == 0) return SPEC_OK;
     if (!x || !h) return SPEC_ERR_NULL;
     if (ld_x % 8 != 0 || ld_h % 8 != 0 || !aligned16(x) || !aligned16(h)) return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
+spec_status check_kv_cache_write(const void* k, int64_t ld_k, const void* v, int64_t ld_v,
+                                 const int64_t* slot_mapping, int64_t T, int64_t H, int64_t D, int64_t num_slots,
+                                 int mode, const float* k_scale, const float* v_scale, const void* k_cache,
+                                 const void* v_cache) {
+    if (mode != SPEC_SCALE_PER_ROW && mode != SPEC_SCALE_PER_TENSOR) return SPEC_ERR_ENUM;
+    if (T < 0 || H <= 0 || D <= 0 || num_slots < 0) return SPEC_ERR_SHAPE;
+    if (H > kMaxGrid || D > 512 || D % 8 != 0) return SPEC_ERR_UNSUPPORTED;
+    if (ld_k < H * D || ld_v < H * D) return SPEC_ERR_SHAPE;
+    if (T > kMaxGrid || num_slots > INT64_MAX / (H * D)) return SPEC_ERR_UNSUPPORTED;
+    int64_t g = 1;                               // lanes per (token, head) row
+    while (g * 8 < D) g *= 2;
+    if ((T * H + 256 / g - 1) / (256 / g) > kMaxGrid) return SPEC_ERR_UNSUPPORTED;
+    if (T == 0) return SPEC_OK;
+    if (!k || !v || !slot_mapping || !k_scale || !v_scale || !k_cache || !v_cache) return SPEC_ERR_NULL;
+    if (ld_k % 8 != 0 || ld_v % 8 != 0 || !aligned16(k) || !aligned16(v)) return SPEC_ERR_ALIGN;
+    if (!aligned16(k_cache) || !aligned16(v_cache)) return SPEC_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(slot_mapping) & 7u) != 0) return SPEC_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(k_scale) & 3u) != 0 || (reinterpret_cast<uintptr_t>(v_scale) & 3u) != 0)
+        return SPEC_ERR_ALIGN;
     return SPEC_OK;
 }
 

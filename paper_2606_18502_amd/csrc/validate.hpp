@@ -17,6 +17,10 @@ spec_status check_silu_mul(const void* x, int64_t rows, int64_t cols, int64_t ld
 spec_status check_gemm(const void* a, int64_t lda, const float* a_scale, int a_mode, const void* w,
                        int64_t ldw, const float* w_scale, int w_mode, int64_t M, int64_t N, int64_t K,
                        const void* y, int64_t ldy, int out_dtype);
+spec_status check_kv_cache_write(const void* k, int64_t ld_k, const void* v, int64_t ld_v,
+                                 const int64_t* slot_mapping, int64_t T, int64_t H, int64_t D, int64_t num_slots,
+                                 int mode, const float* k_scale, const float* v_scale, const void* k_cache,
+                                 const void* v_cache);
 spec_status check_logit_stats(int64_t M, int64_t V, float temperature, const void* logits, int64_t ld_logits,
                               const float* stats, int64_t ld_stats, int64_t n_groups);
 spec_status check_accept_stats(const float* target_stats, int64_t n_stats, int64_t ld_stats, int64_t B);

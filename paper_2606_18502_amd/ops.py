@@ -99,6 +99,55 @@ def silu_mul(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tenso
     return out
 
 
+def kv_cache_write(k: torch.Tensor, v: torch.Tensor, slot_mapping: torch.Tensor, k_cache: torch.Tensor,
+                   v_cache: torch.Tensor, k_scale: torch.Tensor, v_scale: torch.Tensor,
+                   per_tensor: bool = False) -> None:
+    """Quantize new keys and values to E4M3 into the FP8 KV cache (spec_fp8_kv_cache_write).
+
+    k, v: bf16 [T, H, D] views (unit stride over D and heads packed side by
+    side, e.g. column blocks of the QKV output viewed as [T, H, D]);
+    slot_mapping: int64 [T] (negative = skip); k_cache, v_cache: uint8
+    [num_slots, H, D] contiguous (a paged [blocks, block_size, H, D] cache
+    viewed flat).  Per-row scales: k_scale, v_scale fp32 [num_slots, H],
+    written at the stored slots; per_tensor=True: fp32 [1], read.
+    """
+    lib = _lib.load()
+    _dev(k, torch.bfloat16, "k")
+    _dev(v, torch.bfloat16, "v")
+    _dev(slot_mapping, torch.int64, "slot_mapping")
+    _dev(k_cache, torch.uint8, "k_cache")
+    _dev(v_cache, torch.uint8, "v_cache")
+    _dev(k_scale, torch.float32, "k_scale")
+    _dev(v_scale, torch.float32, "v_scale")
+    if k.dim() != 3 or v.shape != k.shape:
+        raise ValueError("k and v must be [T, H, D] of the same shape")
+    T, H, D = k.shape
+    for name, t in (("k", k), ("v", v)):
+        if (D > 1 and t.stride(2) != 1) or (H > 1 and t.stride(1) != D):
+            raise ValueError(f"{name} must have unit stride over D and heads packed side by side")
+    if k_cache.dim() != 3 or k_cache.shape[1:] != (H, D) or v_cache.shape != k_cache.shape \
+            or not k_cache.is_contiguous() or not v_cache.is_contiguous():
+        raise ValueError("k_cache and v_cache must be contiguous [num_slots, H, D]")
+    if slot_mapping.shape != (T,) or not slot_mapping.is_contiguous():
+        raise ValueError("slot_mapping must be a contiguous int64 [T]")
+    num_slots = k_cache.shape[0]
+    if per_tensor:
+        if k_scale.numel() != 1 or v_scale.numel() != 1:
+            raise ValueError("per-tensor scales hold one fp32 value each")
+        mode = _lib.SCALE_PER_TENSOR
+    else:
+        if k_scale.shape != (num_slots, H) or v_scale.shape != (num_slots, H) \
+                or not k_scale.is_contiguous() or not v_scale.is_contiguous():
+            raise ValueError("per-row scales must be contiguous fp32 [num_slots, H]")
+        mode = _lib.SCALE_PER_ROW
+    ld_k = k.stride(0) if T > 1 else H * D
+    ld_v = v.stride(0) if T > 1 else H * D
+    check("spec_fp8_kv_cache_write",
+          lib.spec_fp8_kv_cache_write(k.data_ptr(), ld_k, v.data_ptr(), ld_v, slot_mapping.data_ptr(), T, H, D,
+                                      num_slots, mode, k_scale.data_ptr(), v_scale.data_ptr(),
+                                      k_cache.data_ptr(), v_cache.data_ptr(), _stream()))
+
+
 def gemm_workspace_bytes(M: int, N: int, K: int) -> int:
     return int(_lib.load().spec_fp8_gemm_workspace_bytes(M, N, K))
 

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.spec_version() == 400
+    assert lib.spec_version() == 410
     for s in range(9):
         assert lib.spec_status_string(s)
     assert lib.spec_status_string(99) == b"unknown status"
@@ -74,6 +74,41 @@ def test_quantize_validation(lib):
     assert q(lib, mode=2, scales=None, qp=None, ld_q=0) == NULL
     assert q(lib, mode=2, x=A1, qp=None, ld_q=0) == ALIGN
     assert q(lib, mode=2, ld_x=32, qp=None, ld_q=0) == SHAPE
+
+
+def kv(lib, k=A16, ld_k=1024, v=A16, ld_v=1024, slots=A16, T=4, H=8, D=128, num_slots=64, mode=0,
+       ks=A16, vs=A16, kc=A16, vc=A16):
+    return lib.spec_fp8_kv_cache_write(k, ld_k, v, ld_v, slots, T, H, D, num_slots, mode, ks, vs, kc, vc, None)
+
+
+def test_kv_cache_write_validation(lib):
+    assert kv(lib, mode=2) == ENUM                    # calibration is spec_fp8_quantize's
+    assert kv(lib, mode=7) == ENUM
+    assert kv(lib, T=-1) == SHAPE
+    assert kv(lib, H=0) == SHAPE
+    assert kv(lib, D=0) == SHAPE
+    assert kv(lib, num_slots=-1) == SHAPE
+    assert kv(lib, ld_k=1016) == SHAPE                # ld < H*D
+    assert kv(lib, ld_v=8) == SHAPE
+    assert kv(lib, D=100, ld_k=800, ld_v=800) == UNSUP  # D % 8
+    assert kv(lib, D=520, ld_k=4160, ld_v=4160) == UNSUP  # D > 512
+    assert kv(lib, H=(1 << 31), D=8, ld_k=1 << 34, ld_v=1 << 34) == UNSUP
+    assert kv(lib, num_slots=(1 << 62)) == UNSUP      # cache bytes beyond int64
+    assert kv(lib, k=None) == NULL
+    assert kv(lib, v=None) == NULL
+    assert kv(lib, slots=None) == NULL
+    assert kv(lib, ks=None) == NULL
+    assert kv(lib, vs=None) == NULL
+    assert kv(lib, kc=None) == NULL
+    assert kv(lib, vc=None) == NULL
+    assert kv(lib, k=A1) == ALIGN
+    assert kv(lib, v=A16 + 8) == ALIGN
+    assert kv(lib, ld_k=1028) == ALIGN
+    assert kv(lib, kc=A16 + 8) == ALIGN
+    assert kv(lib, slots=A16 + 4) == ALIGN
+    assert kv(lib, ks=A16 + 2) == ALIGN
+    assert kv(lib, T=0, k=None, v=None, slots=None, ks=None, vs=None, kc=None, vc=None) == OK  # no-op
+    assert kv(lib, num_slots=0) == OK                 # every token skipped: nothing enqueued
 
 
 def test_silu_mul_validation(lib):
