@@ -278,6 +278,112 @@ def tree_parts(torch, p, wl, reps=12):
     return res
 
 
+def draft_and_kv_parts(torch, p, wl, step, reps=22, copies=2):
+    """Two further FP8 uses of the paper, timed like time_parts.
+
+    Drafter: the five FP8 linears of one draft step of the EAGLE-style
+    drafter (feature fc 8192->4096 and one decoder layer, ~250M parameters)
+    over M = 64 rows, with static per-tensor activation scales (calibrated
+    once on the bench inputs before timing) and per-channel weights; each
+    linear is quantize + GEMM, the down projection takes the SiLU-gated
+    quantize of the gate|up output.  Two weight copies are rotated.
+
+    Both are timed as HIP-graph replays (several calls per graph): these
+    kernels take a few microseconds, less than the host needs to issue them
+    eagerly.
+
+    KV cache: the verify step's 320 new tokens, 8 KV heads of 128 read in
+    place from the K and V column blocks of the QKV GEMM output, quantized
+    to E4M3 (per-row scales) into a paged cache of 16-token blocks."""
+    cd = wl.CONFIGS["DRAFT"]
+    M = cd["M"]
+    lin = {name: (N, K) for name, N, K in cd["linears"]}
+    dev = "cuda"
+
+    def bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    acts = {n: bf16(wl.linear_activations(M, K, cd["seed"] + i, cd["act_outlier_frac"], cd["act_outlier_scale"]))
+            for i, (n, (N, K)) in enumerate(lin.items()) if n != "down"}
+    wcopies = []
+    for c in range(copies):
+        ws = {}
+        for i, (n, (N, K)) in enumerate(lin.items()):
+            wb = bf16(wl.linear_weights(N, K, cd["seed"] + 31 + 101 * i + 7919 * c, cd["w_std"]))
+            ws[n] = p.quantize(wb)
+            del wb
+        wcopies.append(ws)
+    q = {n: torch.empty((M, K), dtype=torch.uint8, device=dev) for n, (N, K) in lin.items()}
+    y = {n: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for n, (N, K) in lin.items()}
+    gws = torch.empty((max(16, max(p.gemm_workspace_bytes(M, N, K) for N, K in lin.values())),),
+                      dtype=torch.uint8, device=dev)
+    scale = {n: torch.zeros(1, dtype=torch.float32, device=dev) for n in lin}
+    for n in acts:
+        p.calibrate(acts[n], scale[n])
+    p.gemm(p.quantize(acts["gate_up"], per_tensor_scale=scale["gate_up"])[0], scale["gate_up"],
+           *wcopies[0]["gate_up"], out=y["gate_up"], workspace=gws)
+    p.calibrate(y["gate_up"], scale["down"], silu_mul=True)
+
+    def draft_step(ws):
+        for n in ("fc", "qkv", "o", "gate_up"):
+            p.quantize(acts[n], per_tensor_scale=scale[n], out=q[n])
+            p.gemm(q[n], scale[n], *ws[n], out=y[n], workspace=gws)
+        p.quantize(y["gate_up"], per_tensor_scale=scale["down"], silu_mul=True, out=q["down"])
+        p.gemm(q["down"], scale["down"], *ws["down"], out=y["down"], workspace=gws)
+
+    ck = wl.CONFIGS["KV"]
+    B, T, H, D, bs = ck["B"], ck["T"], ck["H"], ck["D"], ck["block_size"]
+    rng = np.random.default_rng(ck["seed"])
+    ctx = rng.integers(ck["ctx_min"], ck["ctx_max"] + 1, size=B)
+    slots, num_slots = wl.paged_slot_mapping(B, T // B, ctx, bs, seed=ck["seed"] + 1)
+    dslots = torch.from_numpy(slots).to(dev)
+    qkv = step.y["qkv"]
+    qc = qkv.shape[1] - 2 * H * D
+    kx = qkv[:, qc:qc + H * D].view(T, H, D)
+    vx = qkv[:, qc + H * D:].view(T, H, D)
+    kc = torch.zeros((num_slots, H, D), dtype=torch.uint8, device=dev)
+    vc = torch.zeros_like(kc)
+    ks = torch.zeros((num_slots, H), dtype=torch.float32, device=dev)
+    vs = torch.zeros_like(ks)
+
+    def timed(fn, per_graph):
+        """Mean GPU time of fn: `per_graph` calls captured in one HIP graph
+        (launch overhead of the host is not in it), replayed `reps` times."""
+        fn(0)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for r in range(per_graph):
+                fn(r)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * per_graph)
+
+    draft_us = timed(lambda r: draft_step(wcopies[r % copies]), 2 * copies)
+    kv_us = timed(lambda r: p.kv_cache_write(kx, vx, dslots, kc, vc, ks, vs), 20)
+    flops = sum(2.0 * M * N * K for N, K in lin.values())
+    wbytes = sum(N * K + 4 * N for N, K in lin.values())
+    kv_bytes = 2 * T * H * D * (2 + 1) + 2 * T * H * 4 + 8 * T
+    del wcopies, kc, vc
+    return {
+        "drafter_step_us": round(draft_us, 1),
+        "drafter_step_tflops": round(flops / (draft_us * 1e-6) / 1e12, 1),
+        "drafter_weight_gbps": round(wbytes / (draft_us * 1e-6) / 1e9, 1),
+        "drafter_workload": f"drafter linears fc 8192->4096, QKV, O, gate|up, SiLU-gated down at M={M}, static "
+                            f"per-tensor activation scales ({wbytes / 1e6:.1f} MB of FP8 weights per step)",
+        "kv_cache_write_us": round(kv_us, 2),
+        "kv_cache_write_gbps": round(kv_bytes / (kv_us * 1e-6) / 1e9, 1),
+        "kv_workload": f"FP8 KV-cache write of T={T} tokens, {H} heads x {D}, per-row scales, paged "
+                       f"{bs}-token blocks over {num_slots} slots",
+    }
+
+
 def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40):
     """The oracle on the host cores, on a bounded sample of the benched step:
     the 4 linears at M=320 restricted to every `nfrac`-th output channel
@@ -450,6 +556,8 @@ def main(argv=None):
     vendor = vendor_gemm(torch, step, weights)
     lm = lm_head_parts(torch, p, wl)
     tree = tree_parts(torch, p, wl)
+    more = draft_and_kv_parts(torch, p, wl, step)
+    log(f"drafter step {more['drafter_step_us']} us; KV-cache write {more['kv_cache_write_us']} us")
     log(f"tree verification: greedy {tree['greedy_us']} us, sampling {tree['sampling_us']} us")
     log(f"LM head: gemm {lm['gemm']} us (with statistics {lm['gemm_with_stats']}); accept {lm['accept']} us "
         f"(from statistics {lm['accept_from_stats']}); unfused {lm['unfused_us']} us, fused {lm['fused_us']} us")
@@ -485,6 +593,7 @@ def main(argv=None):
             "part_us_p10_p90": spread,
             "lm_head_and_accept_us": lm,
             "tree_accept": tree,
+            "drafter_and_kv_cache": more,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),

@@ -189,3 +189,43 @@ def test_layer_linears_full_size_sampled(cfg):
         bound = error_bound(qa_ref, sa_ref, qw_ref, sw_ref, np.arange(len(rows)), np.arange(len(cols)))
         assert np.all(np.abs(y[np.ix_(rows, cols)] - y_ref) <= bound)
         del x, wt, a, w
+
+
+def test_drafter_linears_static_scales_sampled():
+    """The drafter's five FP8 linears at one draft step (M = 64 rows), with
+    the paper's static per-tensor activation scales: each scale is calibrated
+    on the device over seeded calibration batches (bit-exact against the
+    oracle's min-max calibration), a held-out batch is quantized with it
+    (sampled rows' codes bit-exact), and sampled GEMM outputs match the
+    oracle's exact GEMM to the tolerance and the accumulation bound."""
+    p = need_gpu()
+    c = wl.CONFIGS["DRAFT"]
+    M = c["M"]
+    rows = np.array([0, 1, M // 2, M - 1])
+    for i, (name, N, K) in enumerate(c["linears"]):
+        say(f"drafter {name}: M={M} N={N} K={K}")
+        seed = c["seed"] + 100 * i
+        cal = [wl.linear_activations(M, K, seed + 1 + j, c["act_outlier_frac"], c["act_outlier_scale"])
+               for j in range(c["n_calib"])]
+        run = torch.zeros(1, dtype=torch.float32, device="cuda")
+        for xb in cal:
+            p.calibrate(dev_bf16(xb), run)
+        s_ref = oq.calibrate_per_tensor(cal)
+        assert host(run)[0] == s_ref
+        xb = wl.linear_activations(M, K, seed, c["act_outlier_frac"], c["act_outlier_scale"])
+        wb = wl.linear_weights(N, K, seed + 17, c["w_std"])
+        a, sa = p.quantize(dev_bf16(xb), per_tensor_scale=run)
+        w, sw = p.quantize(dev_bf16(wb))
+        y = host(p.gemm(a, sa, w, sw, out_dtype=torch.float32))
+        rng = np.random.default_rng(N + K)
+        cols = np.unique(np.concatenate([[0, N - 1], rng.choice(N, 256, replace=False)]))
+        qa_ref = oq.quantize_per_tensor(xb[rows], s_ref)
+        sa_ref = np.full(len(rows), s_ref, np.float32)
+        qw_ref, sw_ref = oq.quantize_rows(wb[cols])
+        np.testing.assert_array_equal(host(a)[rows], qa_ref)
+        np.testing.assert_array_equal(host(w)[cols], qw_ref)
+        np.testing.assert_array_equal(host(sw)[cols], sw_ref)
+        y_ref = og.gemm(qa_ref, sa_ref, qw_ref, sw_ref)
+        assert og.rel_error(y[np.ix_(rows, cols)], y_ref) <= TOL
+        bound = error_bound(qa_ref, sa_ref, qw_ref, sw_ref, np.arange(len(rows)), np.arange(len(cols)))
+        assert np.all(np.abs(y[np.ix_(rows, cols)] - y_ref) <= bound)

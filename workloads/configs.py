@@ -61,6 +61,13 @@ CONFIGS = {
         B=64, k=4, V=VOCAB, logit_std=3.0, rank=8, temperature=0.7,
         seed=7, draft_seed=8, uniform_seed=7,
     ),
+    "DRAFT": dict(
+        desc="FP8 linears of the EAGLE-style drafter (the feature fc 8192->4096 plus one "
+             "Llama-3.1-8B-shaped decoder layer, about 250M parameters) for one draft step of "
+             "B=64 sequences (M=64), static per-tensor activation scales from min-max calibration",
+        B=64, M=64, linears=(("fc", HIDDEN, 2 * HIDDEN),) + LAYER_LINEARS, n_calib=8,
+        act_outlier_frac=0.005, act_outlier_scale=30.0, w_std=0.02, seed=13,
+    ),
     "KV": dict(
         desc="FP8 KV-cache write of the verify step's new tokens: B=64, k=4 -> T=320 tokens, "
              "8 KV heads of 128 (Llama 3.1 8B), paged cache with 16-token blocks, "
