@@ -233,3 +233,46 @@ def conditional_next(law, first):
 
 __all__ = ["children", "walk", "walk_greedy", "accept_tree_greedy", "accept_tree_stochastic",
            "tree_emitted_law", "marginal_first", "conditional_next", "target_argmax"]
+
+
+def tree_attention_mask(parent):
+    """Ancestor masks and depths of one sequence's tree (N <= 64 nodes).
+
+    The target model scores every node in one pass: the row of node n may
+    attend to the prefix, the last accepted token (the root) and the nodes on
+    the path from the root to n, itself included; no other node (a sibling
+    branch is another continuation).  Returned per node: the set of those
+    tree nodes as bits of an integer (bit j = node j), and the depth (the
+    number of nodes on the path, so node n sits depth positions after the
+    root).  A node whose chain of parents leaves {-1, 0, .., n-1} at any step
+    is unreachable: mask 0, depth 0.
+    """
+    N = len(parent)
+    masks, depths = [], []
+    for n in range(N):
+        m, d, cur, ok = 0, 0, n, True
+        while cur != -1:
+            p = int(parent[cur])
+            if p < -1 or p >= cur:
+                ok = False
+                break
+            m |= 1 << cur
+            d += 1
+            cur = p
+        masks.append(m if ok else 0)
+        depths.append(d if ok else 0)
+    return masks, depths
+
+
+def tree_attention_masks(parents):
+    """tree_attention_mask for a batch: parents int [B, N] -> (masks uint64
+    [B, N], depths int32 [B, N])."""
+    parents = np.asarray(parents)
+    B, N = parents.shape
+    masks = np.zeros((B, N), np.uint64)
+    depths = np.zeros((B, N), np.int32)
+    for b in range(B):
+        m, d = tree_attention_mask(parents[b])
+        masks[b] = np.array(m, dtype=np.uint64)
+        depths[b] = d
+    return masks, depths

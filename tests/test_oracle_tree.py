@@ -112,3 +112,57 @@ def test_sampling_walk_with_certain_tokens():
     # at node 1 (row 2): node 2 (token 2) rejected, node 3 (token 5) accepted; node 3 is a leaf and its
     # row (row 4) puts all mass on 8, the bonus token
     assert path == [1, 3] and toks == [6, 5, 8]
+
+
+def _visible_top_down(parent):
+    """Independent construction of the ancestor sets: node j is visible to
+    every node of its subtree (found by descending through children)."""
+    N = len(parent)
+    vis = [0] * N
+    for j in range(N):
+        stack = [j]
+        while stack:
+            n = stack.pop()
+            vis[n] |= 1 << j
+            stack.extend(ot.children(parent, n))
+    return vis
+
+
+def test_tree_mask_chain_star_and_subtrees():
+    m, d = ot.tree_attention_mask(list(range(-1, 9)))           # a chain of 10
+    assert m == [(1 << (n + 1)) - 1 for n in range(10)] and d == list(range(1, 11))
+    m, d = ot.tree_attention_mask([-1] * 7)                    # a star
+    assert m == [1 << n for n in range(7)] and d == [1] * 7
+    for N, br in ((25, [4, 3, 2, 1]), (64, [2]), (13, [3, 1])):
+        par = wl.tree_shape(N, br)
+        m, d = ot.tree_attention_mask(par)
+        assert m == _visible_top_down(par)
+        assert d == [bin(x).count("1") for x in m]
+    m, d = ot.tree_attention_mask(wl.TREE25)
+    assert max(d) >= 3 and m == _visible_top_down(wl.TREE25)
+
+
+def test_tree_mask_invalid_parents():
+    par = [-1, 0, 5, 1, -3, 4, 2]      # node 2's parent lies after it; node 4's is below -1
+    m, d = ot.tree_attention_mask(par)
+    assert m[:2] == [1, 3] and m[3] == 0b1011 and d[3] == 3
+    assert m[2] == 0 and m[4] == 0 and d[2] == d[4] == 0
+    assert m[5] == 0 and m[6] == 0     # their descendants are unreachable too
+
+
+def test_accepted_path_is_the_mask_of_its_last_node():
+    B, N, V = 16, 25, 300
+    zt, zd = wl.accept_logits(B, N, V, 3, 0.97, scale=2.0)
+    par = np.asarray(wl.TREE25, np.int32)
+    x = wl.tree_tokens_topk(zd, par)
+    parents = np.tile(par, (B, 1))
+    _, nodes, num = ot.accept_tree_greedy(zt, parents, x)
+    masks, depths = ot.tree_attention_masks(parents)
+    assert num.max() >= 2
+    for b in range(B):
+        a = int(num[b])
+        if a == 0:
+            continue
+        last = int(nodes[b, a - 1])
+        bits = [j for j in range(N) if (int(masks[b, last]) >> j) & 1]
+        assert bits == sorted(nodes[b, :a].tolist()) and depths[b, last] == a
