@@ -359,6 +359,33 @@ spec_status spec_verify_accept_tree(const void* target_logits, const int32_t* pa
                                     int32_t* out_tokens, int32_t* accepted_nodes, int32_t* num_accepted,
                                     void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * spec_tree_attention_mask -- the attention mask of B drafted trees for the
+ * target's single scoring pass over every node (tree attention, the EAGLE
+ * tree mode of the appendix's tree versus greedy drafting).
+ *
+ * The row of node n may attend to the prefix, the root (the last accepted
+ * token) and exactly the tree nodes on the path from the root to n, n
+ * included; a node of another branch is another continuation and stays
+ * hidden.  For every node:
+ *
+ *   mask[b,n]  bit j (j < N) set iff node j lies on that path;
+ *   depth[b,n] the number of nodes on it (the node sits depth[b,n] positions
+ *              after the root, which gives its position id).
+ *
+ * A node whose chain of parents leaves [-1, m) at some node m (the encoding
+ * of spec_verify_accept_tree) is unreachable: mask 0 and depth 0, and so is
+ * every node below it.  For an accepted path (accepted_nodes of
+ * spec_verify_accept_tree), the mask of its last node holds exactly the path.
+ *
+ * parents  int32 [B, N] as for spec_verify_accept_tree.
+ * mask     uint64 [B, N] (8-byte aligned); depth int32 [B, N].
+ * Requirements: B >= 0 (0 is a no-op), N >= 1 (SPEC_ERR_SHAPE); N <= 64 and
+ * ceil(B/4) < 2^31 (SPEC_ERR_UNSUPPORTED).
+ */
+spec_status spec_tree_attention_mask(const int32_t* parents, int64_t B, int64_t N, uint64_t* mask, int32_t* depth,
+                                     void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* spec_status_string(spec_status s);
 

@@ -9,7 +9,8 @@ greedy or speculative-sampling acceptance of the drafted tokens.
 Beside the chain verify step it offers the LM-head GEMM with the acceptance
 statistics in its epilogue (gemm_logit_stats, then verify_accept with
 target_stats), the gate|up GEMM with the SiLU gate in its epilogue
-(gemm_silu_mul), token-tree verification (verify_accept_tree) and the
+(gemm_silu_mul), token-tree verification (verify_accept_tree) with its
+attention masks (tree_attention_mask), and the
 FP8 KV-cache write of the new tokens' keys and values (kv_cache_write).
 
 The computation lives in libspecfp8.so (HIP kernels behind the C ABI of
@@ -30,6 +31,7 @@ from .ops import (  # noqa: F401
     verify_accept,
     accept_workspace_bytes,
     verify_accept_tree,
+    tree_attention_mask,
     accept_tree_workspace_bytes,
 )
 

@@ -20,7 +20,7 @@ OUT_BF16, OUT_F32 = 0, 1
 EXPORTS = ("spec_fp8_quantize", "spec_silu_mul_bf16", "spec_fp8_kv_cache_write", "spec_fp8_gemm_workspace_bytes", "spec_fp8_gemm",
            "spec_fp8_gemm_silu_mul", "spec_logit_stats_count", "spec_fp8_gemm_logit_stats",
            "spec_verify_accept_workspace_bytes", "spec_verify_accept", "spec_verify_accept_stats",
-           "spec_verify_accept_tree_workspace_bytes", "spec_verify_accept_tree",
+           "spec_verify_accept_tree_workspace_bytes", "spec_verify_accept_tree", "spec_tree_attention_mask",
            "spec_status_string", "spec_last_hip_error", "spec_version")
 
 _lib = None
@@ -67,6 +67,8 @@ def load() -> ctypes.CDLL:
     lib.spec_verify_accept_tree_workspace_bytes.restype = sz
     lib.spec_verify_accept_tree.argtypes = [vp, vp, vp, vp, i64, i64, i64, f32, vp, vp, vp, vp, sz, vp]
     lib.spec_verify_accept_tree.restype = i32
+    lib.spec_tree_attention_mask.argtypes = [vp, i64, i64, vp, vp, vp]
+    lib.spec_tree_attention_mask.restype = i32
     lib.spec_verify_accept_workspace_bytes.argtypes = [i64, i64, i64]
     lib.spec_verify_accept_workspace_bytes.restype = sz
     lib.spec_verify_accept.argtypes = [vp, vp, vp, vp, i64, i64, i64, f32, vp, vp, vp, sz, vp]

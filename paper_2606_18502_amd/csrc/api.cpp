@@ -184,6 +184,13 @@ spec_status spec_verify_accept_tree(const void* target_logits, const int32_t* pa
                                                 num_accepted, workspace, as_stream(stream)));
 }
 
+spec_status spec_tree_attention_mask(const int32_t* parents, int64_t B, int64_t N, uint64_t* mask, int32_t* depth,
+                                     void* stream) {
+    const spec_status st = specfp8::check_tree_mask(parents, B, N, mask, depth);
+    if (st != SPEC_OK || B == 0) return st;
+    return from_hip(specfp8::launch_tree_mask(parents, B, N, mask, depth, as_stream(stream)));
+}
+
 const char* spec_status_string(spec_status s) {
     switch (s) {
         case SPEC_OK: return "ok";
@@ -201,6 +208,6 @@ const char* spec_status_string(spec_status s) {
 
 int spec_last_hip_error(void) { return g_last_hip_error; }
 
-int spec_version(void) { return 410; }
+int spec_version(void) { return 500; }
 
 }  // extern "C"

@@ -69,4 +69,10 @@ hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int
                               int32_t* out_tokens, int32_t* accepted_nodes, int32_t* num_accepted, void* workspace,
                               hipStream_t stream);
 
+// ---- tree_mask.hip
+// Ancestor-or-self masks (bit j = node j) and depths of B trees of N <= 64
+// nodes, parents int32 [B][N]; mask uint64 [B][N], depth int32 [B][N].
+hipError_t launch_tree_mask(const int32_t* parents, int64_t B, int64_t N, uint64_t* mask, int32_t* depth,
+                            hipStream_t stream);
+
 }  // namespace specfp8

@@ -67,6 +67,19 @@ spec_status check_kv_cache_write(const void* k, int64_t ld_k, const void* v, int
     return SPEC_OK;
 }
 
+spec_status check_tree_mask(const int32_t* parents, int64_t B, int64_t N, const uint64_t* mask,
+                            const int32_t* depth) {
+    if (B < 0 || N < 1) return SPEC_ERR_SHAPE;
+    if (N > 64) return SPEC_ERR_UNSUPPORTED;
+    if ((B + 3) / 4 > kMaxGrid) return SPEC_ERR_UNSUPPORTED;
+    if (B == 0) return SPEC_OK;
+    if (!parents || !mask || !depth) return SPEC_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(parents) & 3u) != 0 || (reinterpret_cast<uintptr_t>(depth) & 3u) != 0 ||
+        (reinterpret_cast<uintptr_t>(mask) & 7u) != 0)
+        return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
 spec_status check_gemm(const void* a, int64_t lda, const float* a_scale, int a_mode, const void* w,
                        int64_t ldw, const float* w_scale, int w_mode, int64_t M, int64_t N, int64_t K,
                        const void* y, int64_t ldy, int out_dtype) {

@@ -28,6 +28,8 @@ spec_status check_accept_tree(const void* target_logits, const int32_t* parents,
                               const float* uniforms, int64_t B, int64_t N, int64_t V, float temperature,
                               const int32_t* out_tokens, const int32_t* accepted_nodes,
                               const int32_t* num_accepted);
+spec_status check_tree_mask(const int32_t* parents, int64_t B, int64_t N, const uint64_t* mask,
+                            const int32_t* depth);
 spec_status check_accept(const void* target_logits, const void* draft_logits, const int32_t* draft_tokens,
                          const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
                          const int32_t* out_tokens, const int32_t* num_accepted);

@@ -380,3 +380,28 @@ def verify_accept_tree(target_logits: torch.Tensor, parents: torch.Tensor, token
         accepted_nodes.data_ptr(), num_accepted.data_ptr(), workspace.data_ptr(),
         workspace.numel() * workspace.element_size(), _stream()))
     return out_tokens, accepted_nodes, num_accepted
+
+
+def tree_attention_mask(parents: torch.Tensor, mask: Optional[torch.Tensor] = None,
+                        depth: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Ancestor-or-self masks and depths of B drafted trees (spec_tree_attention_mask).
+
+    parents: int32 [B, N] (N <= 64).  Returns (mask int64 [B, N] holding the
+    uint64 bit patterns, bit j = node j; depth int32 [B, N]).
+    """
+    lib = _lib.load()
+    _dev(parents, torch.int32, "parents")
+    if parents.dim() != 2 or not parents.is_contiguous():
+        raise ValueError("parents must be a contiguous int32 [B, N]")
+    B, N = parents.shape
+    if mask is None:
+        mask = torch.empty((B, N), dtype=torch.int64, device=parents.device)
+    if depth is None:
+        depth = torch.empty((B, N), dtype=torch.int32, device=parents.device)
+    _dev(mask, torch.int64, "mask")
+    _dev(depth, torch.int32, "depth")
+    if mask.shape != (B, N) or depth.shape != (B, N) or not mask.is_contiguous() or not depth.is_contiguous():
+        raise ValueError("mask and depth must be contiguous [B, N]")
+    check("spec_tree_attention_mask", lib.spec_tree_attention_mask(parents.data_ptr(), B, N, mask.data_ptr(),
+                                                                   depth.data_ptr(), _stream()))
+    return mask, depth

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.spec_version() == 410
+    assert lib.spec_version() == 500
     for s in range(9):
         assert lib.spec_status_string(s)
     assert lib.spec_status_string(99) == b"unknown status"
@@ -109,6 +109,21 @@ def test_kv_cache_write_validation(lib):
     assert kv(lib, ks=A16 + 2) == ALIGN
     assert kv(lib, T=0, k=None, v=None, slots=None, ks=None, vs=None, kc=None, vc=None) == OK  # no-op
     assert kv(lib, num_slots=0) == OK                 # every token skipped: nothing enqueued
+
+
+def test_tree_mask_validation(lib):
+    f = lib.spec_tree_attention_mask
+    assert f(A16, -1, 5, A16, A16, None) == SHAPE
+    assert f(A16, 4, 0, A16, A16, None) == SHAPE
+    assert f(A16, 4, 65, A16, A16, None) == UNSUP
+    assert f(A16, 1 << 40, 5, A16, A16, None) == UNSUP
+    assert f(None, 4, 5, A16, A16, None) == NULL
+    assert f(A16, 4, 5, None, A16, None) == NULL
+    assert f(A16, 4, 5, A16, None, None) == NULL
+    assert f(A16 + 2, 4, 5, A16, A16, None) == ALIGN
+    assert f(A16, 4, 5, A16 + 4, A16, None) == ALIGN
+    assert f(A16, 4, 5, A16, A16 + 2, None) == ALIGN
+    assert f(None, 0, 5, None, None, None) == OK
 
 
 def test_silu_mul_validation(lib):

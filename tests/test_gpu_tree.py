@@ -168,3 +168,41 @@ def test_tree25_full_vocabulary():
     np.testing.assert_array_equal(out[clear], out_ref[clear])
     np.testing.assert_array_equal(nodes[clear], nodes_ref[clear])
     _check_valid_walk(out, nodes, num, parents, x, V)
+
+
+@pytest.mark.parametrize("B,N,seed", [(1, 1, 0), (7, 7, 1), (301, 25, 2), (33, 64, 3), (5, 40, 4)])
+def test_tree_attention_mask_bit_exact(B, N, seed):
+    """Masks and depths of random trees (some with invalid parents, whose
+    subtrees are unreachable) equal the oracle's, bit for bit."""
+    p = need_gpu()
+    say(f"tree mask B={B} N={N}")
+    rng = np.random.default_rng(seed)
+    parents = np.array([[int(rng.integers(-1, n)) if n else -1 for n in range(N)] for _ in range(B)], np.int32)
+    for b in range(0, B, 3):
+        i = int(rng.integers(0, N))
+        parents[b, i] = int(rng.choice([i, i + 2, -2, 99]))
+    mask, depth = p.tree_attention_mask(dev_i32(parents))
+    ref_m, ref_d = ot.tree_attention_masks(parents)
+    np.testing.assert_array_equal(host(mask).view(np.uint64), ref_m)
+    np.testing.assert_array_equal(host(depth), ref_d)
+
+
+def test_tree_attention_mask_holds_the_accepted_path():
+    """On the device: the mask of the last accepted node of
+    spec_verify_accept_tree is exactly the accepted path, and its depth the
+    path length."""
+    p = need_gpu()
+    B, V = 24, 5000
+    par = np.asarray(wl.TREE25, np.int32)
+    N = len(par)
+    zt, parents, x, u = _case(B, N, V, 21, 0.97, parent=par)
+    out, nodes, num = p.verify_accept_tree(dev_bf16(zt), dev_i32(parents), dev_i32(x), dev_f32(u), 0.7)
+    mask, depth = p.tree_attention_mask(dev_i32(parents))
+    nodes, num, mask, depth = host(nodes), host(num), host(mask).view(np.uint64), host(depth)
+    assert num.max() >= 2
+    for b in range(B):
+        a = int(num[b])
+        if a:
+            last = int(nodes[b, a - 1])
+            bits = [j for j in range(N) if (int(mask[b, last]) >> j) & 1]
+            assert bits == sorted(nodes[b, :a].tolist()) and depth[b, last] == a
