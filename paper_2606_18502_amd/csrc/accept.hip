@@ -390,6 +390,48 @@ __device__ __forceinline__ double range_mass(const Dist& d, float c2, int64_t e0
     return m;
 }
 
+// Masses of the kAThreads ranges of kPerThread elements of chunk ch, read with
+// coalesced loads: wave wv covers the chunk's elements [wv*4096, (wv+1)*4096)
+// in kVecs loads of 512 (16 bytes per lane, consecutive lanes on consecutive
+// 16-byte pieces, so one load instruction reads 1 KiB contiguous).  The 8 lanes
+// that share a range add their sums by xor exchanges in a fixed order, and the
+// first of them stores the mass of range wv*64 + j*8 + lane/8 into s_rm.  Called
+// by the whole block; s_rm is complete after the caller's next barrier.
+template <bool VEC, bool HAS_D>
+__device__ __forceinline__ void chunk_masses(const Dist& d, float c2, int64_t ch, int64_t V, int t,
+                                             double* s_rm) {
+    static_assert(kChunk == (int64_t)kWavesPerBlock * kVecs * kWave * 8 && kPerThread == 8 * 8,
+                  "a range is 8 lanes of one load");
+    const int lane = t & (kWave - 1), wv = t / kWave;
+    const int64_t base = ch * kChunk + (int64_t)wv * (kVecs * kWave * 8) + (int64_t)lane * 8;
+    Raw rt, rd;
+    if (VEC) {
+#pragma unroll
+        for (int j = 0; j < kVecs; ++j) {
+            const int64_t e = base + (int64_t)j * kWave * 8;
+            if (e < V) {
+                rt[j] = *reinterpret_cast<const uint4*>(d.zt_row + e);
+                if (HAS_D) rd[j] = *reinterpret_cast<const uint4*>(d.zd_row + e);
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < kVecs; ++j) {
+        const int64_t e = base + (int64_t)j * kWave * 8;
+        double m = 0.0;
+        if (e < V) {
+            float r[8];
+            dist8<VEC, HAS_D>(d, c2, rt[j], rd[j], e, V, r);
+            m = (((double)r[0] + (double)r[1]) + ((double)r[2] + (double)r[3])) +
+                (((double)r[4] + (double)r[5]) + ((double)r[6] + (double)r[7]));
+        }
+        m += __shfl_xor(m, 1);
+        m += __shfl_xor(m, 2);
+        m += __shfl_xor(m, 4);
+        if ((lane & 7) == 0) s_rm[wv * (kVecs * 8) + j * 8 + (lane >> 3)] = m;
+    }
+}
+
 // Block-wide scan of one double per thread, in thread order: the thread's
 // interval [lo, hi) of the running sum and the block total.  Intervals of
 // consecutive threads tile exactly (hi of thread t is bit-identical to lo of
@@ -464,6 +506,7 @@ __device__ __forceinline__ void merge_ms(float& m, float& z, float om, float oz)
 template <bool VEC>
 __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     __shared__ float sM[33], sZ[33];
+    __shared__ double s_rm[kAThreads];
     __shared__ int s_acc[16];
     __shared__ int s_j, s_last;
     __shared__ double sh[kWavesPerBlock];
@@ -576,11 +619,13 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
         e0 = ch * kChunk + (int64_t)th * kPerThread;
         e1 = min(e0 + kPerThread, a.V);
     };
+    // the mass of this thread's range of chunk ch (every thread of the block calls it)
     auto mass_of = [&](int64_t ch) {
-        int64_t e0, e1;
-        range_of(ch, t, e0, e1);
-        if (e0 >= a.V) return 0.0;
-        return d.zd_row ? range_mass<VEC, true>(d, a.c2, e0, e1) : range_mass<VEC, false>(d, a.c2, e0, e1);
+        __syncthreads();                     // s_rm's previous readers are done
+        if (d.zd_row) chunk_masses<VEC, true>(d, a.c2, ch, a.V, t, s_rm);
+        else chunk_masses<VEC, false>(d, a.c2, ch, a.V, t, s_rm);
+        __syncthreads();
+        return s_rm[t];
     };
 
     // 3. this block's range masses and chunk total, stored device-coherently
