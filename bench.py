@@ -384,6 +384,78 @@ def draft_and_kv_parts(torch, p, wl, step, reps=22, copies=2):
     }
 
 
+def quantize_parts(torch, p, wl, step, reps=12):
+    """Per-token quantize bandwidth.  At the verify step's M = 320 rows a call
+    moves 2-23 MB and is bound by latency; the long-prompt rows of the C5
+    configuration (M = 4096: X [4096, 4096] and the FFN intermediate
+    [4096, 14336], bf16 in, E4M3 codes and fp32 scales out) are large enough
+    to be bound by HBM.  Each C5 shape rotates enough input copies to exceed
+    the 256 MB Infinity Cache; timed as HIP-graph replays."""
+    c5 = wl.CONFIGS["C5"]
+    M = c5["M"]
+    res = {}
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(55)
+    for name, K in (("x_4096x4096", c5["K1"]), ("h_4096x14336", c5["K2"])):
+        ncp = max(2, int(np.ceil(300e6 / (2.0 * M * K))))
+        xs = [torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16) for _ in range(ncp)]
+        q = torch.empty((M, K), dtype=torch.uint8, device="cuda")
+        sc = torch.empty((M,), dtype=torch.float32, device="cuda")
+        s1 = torch.ones(1, dtype=torch.float32, device="cuda")
+        for mode in ("per_token", "static"):
+            def call(r, mode=mode):
+                if mode == "per_token":
+                    p.quantize(xs[r % ncp], out=q, scales=sc)
+                else:
+                    p.quantize(xs[r % ncp], per_tensor_scale=s1, out=q)
+            call(0)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for r in range(ncp):
+                    call(r)
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / (reps * ncp)
+            nbytes = 3.0 * M * K + (4.0 * M if mode == "per_token" else 4.0)
+            res[f"{name}_{mode}_us"] = round(us, 2)
+            res[f"{name}_{mode}_gbps"] = round(nbytes / (us * 1e-6) / 1e9, 1)
+            res[f"{name}_{mode}_pct_hbm_peak"] = round(100 * nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1)
+        del xs
+    # the verify step's own calls (M = 320), as graph replays too: eager
+    # launches of a few-microsecond kernel measure the host, not the GPU
+    for name in ("qkv", "gate_up_silu"):
+        def call(name=name):
+            if name == "qkv":
+                p.quantize(step.acts["qkv"], out=step.q["qkv"], scales=step.s["qkv"])
+            else:
+                p.quantize(step.y["gate_up"], silu_mul=True, out=step.q["down"], scales=step.s["down"])
+        call()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(10):
+                call()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        res[f"verify_{name}_us"] = round(e0.elapsed_time(e1) * 1e3 / (reps * 10), 2)
+    res["workload"] = ("per-token E4M3 quantize of bf16 rows: C5 long-prompt shapes M=4096 (HBM-bound), "
+                       "and the verify step's M=320 calls (latency-bound)")
+    return res
+
+
 def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40):
     """The oracle on the host cores, on a bounded sample of the benched step:
     the 4 linears at M=320 restricted to every `nfrac`-th output channel
@@ -557,6 +629,9 @@ def main(argv=None):
     lm = lm_head_parts(torch, p, wl)
     tree = tree_parts(torch, p, wl)
     more = draft_and_kv_parts(torch, p, wl, step)
+    quant = quantize_parts(torch, p, wl, step)
+    log(f"quantize C5 4096x14336 per-token {quant['h_4096x14336_per_token_us']} us "
+        f"({quant['h_4096x14336_per_token_pct_hbm_peak']}% of HBM peak)")
     log(f"drafter step {more['drafter_step_us']} us; KV-cache write {more['kv_cache_write_us']} us")
     log(f"tree verification: greedy {tree['greedy_us']} us, sampling {tree['sampling_us']} us")
     log(f"LM head: gemm {lm['gemm']} us (with statistics {lm['gemm_with_stats']}); accept {lm['accept']} us "
@@ -594,6 +669,7 @@ def main(argv=None):
             "lm_head_and_accept_us": lm,
             "tree_accept": tree,
             "drafter_and_kv_cache": more,
+            "quantize": quant,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),
