@@ -72,6 +72,8 @@ struct GemmArgs {
     int stats_mode;   // 0: none; 1: (max t, sum 2^(t - max)), t = z * c2; 2: (max z, lowest column)
     float c2;
     int silu_inter;   // > 0: SiLU-gated output of I = silu_inter columns from W = [gate; up] (N = 2I)
+    int group_m;      // > 1: tiles are ordered in groups of group_m M-tiles that walk the N-tiles together
+    int krot_on;      // 1: workgroups of different N-tiles start K at staggered steps
 };
 
 // Weight row of logical output column n.  With the SiLU-gated epilogue every
@@ -507,8 +509,21 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     // consecutive logical ids: K-splits of a tile, then M-tiles of an N-tile
     const int split = logical % g.splits;
     const int tile = logical / g.splits;
-    const int mt = tile % g.m_tiles;
-    const int nt = tile / g.m_tiles;
+    int mt, nt;
+    if (g.group_m > 1) {
+        // Large M: a group of group_m M-tiles walks the N-tiles, so the tiles
+        // that run at once on one XCD form a group_m x (CUs / group_m) block
+        // and re-read each other's operand rows from that XCD's L2.
+        const int per_group = g.group_m * g.n_tiles;
+        const int first = (tile / per_group) * g.group_m;
+        const int gm = min(g.group_m, g.m_tiles - first);
+        const int in = tile - (tile / per_group) * per_group;
+        mt = first + in % gm;
+        nt = in / gm;
+    } else {
+        mt = tile % g.m_tiles;
+        nt = tile / g.m_tiles;
+    }
     const int m0 = mt * C::BM;
     const int n0 = nt * C::BN;
 
@@ -518,7 +533,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     const int nk = ks1 - ks0;
     // Workgroups that share an activation tile walk K from different
     // starting points, so they do not all request the same bytes at once.
-    const int krot = (nt * 7 + split) % nk;
+    const int krot = g.krot_on ? (nt * 7 + split) % nk : 0;
 
     v4f acc[WTN][WTM];
 #pragma unroll
@@ -722,6 +737,20 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     // every split must own at least one K-step after ceil division
     while (splits > 1 && (int64_t)((ksteps + splits - 1) / splits) * (splits - 1) >= ksteps) --splits;
     p.splits = splits;
+    // Many M-tiles (long prompts): tiles in groups of 4 M-tiles with K walked
+    // in step, so the 32 tiles an XCD runs at once re-read 4 activation and
+    // 8 weight tiles from its L2 (5-8% at M = 4096).  Few M-tiles keep the
+    // staggered K start, which spreads the requests for shared rows.
+    p.group_m = 1;
+    p.krot_on = 1;
+    if (p.m_tiles >= 8 && splits == 1) {
+        p.group_m = 4;
+        p.krot_on = 0;
+    }
+#ifdef SPECFP8_TUNING
+    if (const char* env = getenv("SPECFP8_GROUP_M")) p.group_m = atoi(env) > 0 ? atoi(env) : 1;
+    if (const char* env = getenv("SPECFP8_KROT")) p.krot_on = atoi(env);
+#endif
     p.stat_groups = (int64_t)p.n_tiles * kCfgWN[p.kind];
     p.ldp = (N + 3) / 4 * 4;
     p.workspace_bytes = splits > 1 ? (size_t)splits * (size_t)M * (size_t)p.ldp * sizeof(float) : 0;
@@ -742,6 +771,8 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
     g.M = (int)M; g.N = (int)N; g.K = (int)K;
     g.a_per_tensor = a_per_tensor; g.w_per_tensor = w_per_tensor; g.out_f32 = out_f32;
     g.m_tiles = p.m_tiles; g.n_tiles = p.n_tiles; g.splits = p.splits; g.ksteps = (int)(K / kBK);
+    g.group_m = p.group_m;
+    g.krot_on = p.krot_on;
     hipError_t e;
     switch (p.kind) {
         case 0: e = launch_cfg<Cfg0, 2, 2, 2, 2, 4>(g, stream); break;

@@ -27,6 +27,8 @@ struct GemmPlan {
     int kind;              // tile configuration
     int m_tiles, n_tiles;  // output tiles
     int splits;            // K-splits (1 = none)
+    int group_m;           // > 1: tile order in groups of group_m M-tiles
+    int krot_on;           // staggered K start per N-tile
     int64_t stat_groups;   // column groups per row of the epilogue statistics (n_tiles * waves across N)
     int64_t ldp;           // row stride of the fp32 partial tiles
     size_t workspace_bytes;

@@ -56,6 +56,7 @@ def _sample(n, count, seed):
     (320, 640, 4096), (333, 272, 2048),                    # 320-row tile, split-K, ragged M
     (300, 1000, 1024),                                     # 64x128 tile, ragged M and N, split-K
     (700, 400, 512), (1024, 1024, 1024),                   # 256-row tile
+    (1300, 672, 256), (1777, 100, 128),                    # >= 8 M-tiles: grouped tile order, ragged group
 ])
 def test_gemm_parity(M, N, K):
     p = need_gpu()
