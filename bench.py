@@ -553,6 +553,24 @@ def profile_traffic(torch, p, wl):
     return 0
 
 
+def profile_gemm_c5(torch, p, wl):
+    """Kernels for counter passes on the long-prompt GEMM: three launches of
+    the C5 up projection (M = 4096, 4096 -> 14336) on different weight copies."""
+    c5 = wl.CONFIGS["C5"]
+    M, K, N = c5["M"], c5["K1"], c5["N1"]
+    a = torch.randint(0, 120, (M, K), dtype=torch.uint8, device="cuda")
+    sa = torch.rand(M, device="cuda") * 0.01 + 1e-3
+    ws = [torch.randint(0, 120, (N, K), dtype=torch.uint8, device="cuda") for _ in range(3)]
+    sw = torch.rand(N, device="cuda") * 0.01 + 1e-3
+    out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    wsb = torch.empty((max(p.gemm_workspace_bytes(M, N, K), 16),), dtype=torch.uint8, device="cuda")
+    for i in range(3):
+        p.gemm(a, sa, ws[i], sw, out=out, workspace=wsb)
+    torch.cuda.synchronize()
+    log("profile kernels done")
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -560,9 +578,10 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--copies", type=int, default=3, help="rotated copies of weights and logits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile", choices=["traffic"], default=None,
-                    help="for hardware-counter runs: a plain copy of 256 MiB (the counters' calibration), then "
-                         "3 launches of the gate|up GEMM, then exit")
+    ap.add_argument("--profile", choices=["traffic", "gemm_c5"], default=None,
+                    help="for hardware-counter runs: 'traffic' = a plain copy of 256 MiB (the counters' "
+                         "calibration), then 3 launches of the gate|up GEMM; 'gemm_c5' = 3 launches of the "
+                         "M=4096 4096->14336 GEMM; then exit")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}): the verify path runs on one "
@@ -580,6 +599,8 @@ def main(argv=None):
     torch.cuda.set_device(0)
     if args.profile == "traffic":
         return profile_traffic(torch, p, wl)
+    if args.profile == "gemm_c5":
+        return profile_gemm_c5(torch, p, wl)
     acts, weights, logits = build_inputs(torch, p, wl, args.copies)
     step = Step(torch, p, wl, acts)
     cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
