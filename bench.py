@@ -456,6 +456,88 @@ def quantize_parts(torch, p, wl, step, reps=12):
     return res
 
 
+def other_configs(torch, p, wl, reps=12):
+    """The GEMMs of the other layer configurations, for their rooflines.
+
+    C2: the same four linears at M = 80 (B = 16, k = 4), HBM-bound (the
+    weights dominate: 218 MB per layer); weights rotated over enough copies to
+    exceed the Infinity Cache.  C5: the long-prompt FFN GEMMs at M = 4096
+    (4096 -> 14336 and 14336 -> 4096), MFMA-bound, beside hipBLASLt on the
+    same codes.  Per-token activation and per-channel weight scales, bf16 out,
+    timed as HIP-graph replays."""
+    f8 = torch.float8_e4m3fn
+    g = torch.Generator(device="cuda")
+    g.manual_seed(77)
+    res = {}
+
+    def timed(fn, ncalls):
+        """Mean GPU time per call: ncalls calls (cycling over the input copies)
+        captured in one HIP graph and replayed; the host's launch cost of the
+        binding (comparable to these kernels' run time at M = 80) stays out."""
+        fn(0)
+        torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for r in range(ncalls):
+                fn(r)
+        gr.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            gr.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * ncalls)
+
+    c2 = wl.CONFIGS["C2"]
+    M = c2["M"]
+    tot_us, tot_bytes = 0.0, 0.0
+    c2res = {}
+    for name, N, K in c2["linears"]:
+        a, sa = p.quantize(torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16))
+        ncp = max(2, int(np.ceil(300e6 / (N * K))))
+        wq = [p.quantize(torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)) for _ in range(ncp)]
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty((max(16, p.gemm_workspace_bytes(M, N, K)),), dtype=torch.uint8, device="cuda")
+        us = timed(lambda r: p.gemm(a, sa, *wq[r % ncp], out=out, workspace=ws), ncp)
+        nbytes = M * K + N * K + 4 * (M + N) + 2 * M * N
+        c2res[name + "_us"] = round(us, 1)
+        tot_us += us
+        tot_bytes += nbytes
+        del wq
+    c2res["layer_gemm_us"] = round(tot_us, 1)
+    c2res["layer_gbps"] = round(tot_bytes / (tot_us * 1e-6) / 1e9, 1)
+    c2res["layer_pct_hbm_peak"] = round(100 * tot_bytes / (tot_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1)
+    c2res["workload"] = "C2 layer linears at M=80 (B=16, k=4): QKV, O, gate|up, down"
+    res["C2"] = c2res
+
+    c5 = wl.CONFIGS["C5"]
+    M = c5["M"]
+    c5res = {}
+    for name, K, N in (("up", c5["K1"], c5["N1"]), ("down", c5["K2"], c5["N2"])):
+        a, sa = p.quantize(torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16))
+        wq = [p.quantize(torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)) for _ in range(3)]
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty((max(16, p.gemm_workspace_bytes(M, N, K)),), dtype=torch.uint8, device="cuda")
+        fl = 2.0 * M * N * K
+        us = timed(lambda r: p.gemm(a, sa, *wq[r % 3], out=out, workspace=ws), 3)
+        c5res[name + "_us"] = round(us, 1)
+        c5res[name + "_tflops"] = round(fl / (us * 1e-6) / 1e12, 1)
+        c5res[name + "_pct_mfma_peak"] = round(100 * fl / (us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 1)
+        try:
+            vus = timed(lambda r: torch._scaled_mm(a.view(f8), wq[r % 3][0].view(f8).t(), scale_a=sa.view(-1, 1),
+                                                   scale_b=wq[r % 3][1].view(1, -1), out_dtype=torch.bfloat16), 3)
+            c5res[name + "_hipblaslt_us"] = round(vus, 1)
+        except Exception as e:      # a library without this FP8 path
+            log(f"hipBLASLt C5 {name}: {str(e)[:100]}")
+            c5res[name + "_hipblaslt_us"] = None
+        del wq
+    c5res["workload"] = "C5 long-prompt FFN GEMMs at M=4096: 4096->14336 (up) and 14336->4096 (down)"
+    res["C5"] = c5res
+    return res
+
+
 def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40):
     """The oracle on the host cores, on a bounded sample of the benched step:
     the 4 linears at M=320 restricted to every `nfrac`-th output channel
@@ -651,6 +733,9 @@ def main(argv=None):
     tree = tree_parts(torch, p, wl)
     more = draft_and_kv_parts(torch, p, wl, step)
     quant = quantize_parts(torch, p, wl, step)
+    others = other_configs(torch, p, wl)
+    log(f"C2 layer GEMMs {others['C2']['layer_gemm_us']} us ({others['C2']['layer_pct_hbm_peak']}% of HBM peak); "
+        f"C5 up {others['C5']['up_pct_mfma_peak']}%, down {others['C5']['down_pct_mfma_peak']}% of FP8 peak")
     log(f"quantize C5 4096x14336 per-token {quant['h_4096x14336_per_token_us']} us "
         f"({quant['h_4096x14336_per_token_pct_hbm_peak']}% of HBM peak)")
     log(f"drafter step {more['drafter_step_us']} us; KV-cache write {more['kv_cache_write_us']} us")
@@ -691,6 +776,7 @@ def main(argv=None):
             "tree_accept": tree,
             "drafter_and_kv_cache": more,
             "quantize": quant,
+            "other_configs": others,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),

@@ -689,7 +689,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     GemmPlan p{};
     const bool no_split = epilogue != kEpiPlain;
     // Tile shapes by measurement on MI355X (M = B*(k+1) verify rows):
-    //   M <= 64: 64x64;  M <= 80: 80x128;
+    //   M <= 80: 64x64 with K split (below), but for very wide N (gate|up)
+    //            64x128 (M <= 64) or 80x128 unsplit;
     //   M <= 320: 160x224 when N fills >= 64 such columns exactly (gate|up),
     //             else for very wide N (an LM head) 160x192 (or 160x224
     //             with a ragged last tile),
@@ -697,8 +698,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     //             64x128 (QKV, O: a CU's time is set by the operand rows it
     //             streams per K-step, 192 here against 224 for 160x64);
     //   larger M: 160x224.
-    if (M <= 64) p.kind = 0;
-    else if (M <= 80) p.kind = 1;
+    if (M <= 80) p.kind = N >= 192 * 64 ? (M <= 64 ? 8 : 1) : 0;
     else if (M <= 320) {
         if (N % 224 == 0 && N >= 224 * 64) p.kind = 2;
         else if (N >= 192 * 64) p.kind = (N % 192 == 0) ? 4 : 2;
@@ -722,6 +722,17 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     p.n_tiles = (int)((N + bn - 1) / bn);
     const int64_t tiles = (int64_t)p.m_tiles * p.n_tiles;
     if (no_split) splits = 1;
+    if (splits <= 0 && M <= 80 && p.kind == 0) {
+        // Draft and small verify batches (64x64 tiles): the GEMM is a weight
+        // stream with a fixed cost per workgroup, so K is split until about
+        // 256 workgroups run or every split holds at most 32 K-steps, keeping
+        // at least 8 K-steps per split (the partials are small at this M).
+        splits = (int)(256 / tiles);
+        if (splits < (ksteps + 31) / 32) splits = (ksteps + 31) / 32;
+        const int max_split = ksteps / 8 > 0 ? ksteps / 8 : 1;
+        if (splits > max_split) splits = max_split;
+        if (splits > 16) splits = 16;
+    }
     if (splits <= 0) {
         // Split K only when at most half of the 256 compute units would get
         // a tile, and keep the split grid under ~200 workgroups: every split

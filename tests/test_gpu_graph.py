@@ -20,7 +20,7 @@ pytestmark = pytest.mark.gpu
 
 def test_graph_replays_match_eager():
     p = need_gpu()
-    M, K1, N1, K2 = 80, 1024, 2 * 1536, 1536        # gate|up then down (split-K shape)
+    M, K1, N1, K2 = 80, 1024, 2 * 4096, 4096        # gate|up then down (split-K shape)
     N2 = 1024
     B, k, V, T = 8, 3, 20000, 0.7
     dev = "cuda"
