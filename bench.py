@@ -538,38 +538,31 @@ def other_configs(torch, p, wl, reps=12):
     return res
 
 
-def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40):
-    """The oracle on the host cores, on a bounded sample of the benched step:
-    the 4 linears at M=320 restricted to every `nfrac`-th output channel
-    (full K; per-token quantize, the SiLU-gated re-quantize of a full-width
-    gate|up output, exact fp64 GEMMs on the decoded operands) and stochastic
-    acceptance of all 64 sequences at full vocabulary, repeated until at least
-    `min_seconds` have passed.  `value` is GEMM FLOPs per second."""
+def _cpu_sample(wl, nfrac, min_seconds, max_reps):
+    """One oracle pass per repetition over a bounded sample of the benched
+    step: the 4 linears at M=320 restricted to every `nfrac`-th output
+    channel (full K; per-token quantize, the SiLU-gated re-quantize of a
+    full-width gate|up output, exact fp64 GEMMs on the decoded operands) and
+    stochastic acceptance of all 64 sequences at full vocabulary.  One
+    untimed warm-up pass, then at least 3 timed ones, until `min_seconds`
+    have passed (at most `max_reps`).  Returns GEMM FLOPs per pass, the
+    per-pass times and a description."""
     from oracle import accept as oa, gemm as og, quantize as oq
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
-    except Exception:
-        threads = os.cpu_count() or 1
     cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
     M = cfg3["M"]
     xs, wq = {}, {}
     for i, (name, N, K) in enumerate(cfg3["linears"]):
-        if name == "down":
-            xs[name] = wl.linear_activations(M, 2 * K, cfg3["seed"] + i, cfg3["act_outlier_frac"],
-                                             cfg3["act_outlier_scale"])          # gate|up output stand-in
-        else:
-            xs[name] = wl.linear_activations(M, K, cfg3["seed"] + i, cfg3["act_outlier_frac"],
-                                             cfg3["act_outlier_scale"])
+        width = 2 * K if name == "down" else K                      # down: gate|up output stand-in
+        xs[name] = wl.linear_activations(M, width, cfg3["seed"] + i, cfg3["act_outlier_frac"],
+                                         cfg3["act_outlier_scale"])
         wq[name] = oq.quantize_rows(wl.linear_weights(N // nfrac, K, cfg3["seed"] + 17 + 101 * i, cfg3["w_std"]))
     B, k, V, T = cfg4["B"], cfg4["k"], cfg4["V"], cfg4["temperature"]
     zt, zd = wl.accept_logits(B, k, V, cfg4["seed"], wl.C4_CORRELATION, scale=cfg4["logit_std"], rank=cfg4["rank"])
     x = wl.draft_tokens_sampled(zd, T, seed=cfg4["draft_seed"])
     u = wl.philox_uniforms((B, k + 1), seed=cfg4["uniform_seed"])
     flops_rep = sum(2.0 * M * (N // nfrac) * K for _, N, K in cfg3["linears"])
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
+
+    def one_pass():
         for name, N, K in cfg3["linears"]:
             if name == "down":
                 a, sa, _ = oq.quantize_silu_mul_rows(xs[name])
@@ -578,14 +571,84 @@ def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40):
             w, sw = wq[name]
             og.gemm(a, sa, w, sw)
         oa.accept_stochastic(zt, zd, x, u, T)
-        reps += 1
-        dt = time.perf_counter() - t0
-        if dt >= min_seconds or reps >= max_reps:
-            break
-    return {"value": flops_rep * reps / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{reps}x: the 4 layer linears at M={M} on every {nfrac}th output channel (full K; "
-                      f"per-token and SiLU-gated quantize, exact fp64 GEMMs) plus stochastic acceptance of all "
-                      f"{B} sequences at V={V}; {dt:.1f} s"}
+
+    one_pass()                                                      # warm-up
+    times = []
+    t0 = time.perf_counter()
+    while len(times) < 3 or (time.perf_counter() - t0 < min_seconds and len(times) < max_reps):
+        t1 = time.perf_counter()
+        one_pass()
+        times.append(time.perf_counter() - t1)
+    desc = (f"the 4 layer linears at M={M} on every {nfrac}th output channel (full K; per-token and "
+            f"SiLU-gated quantize, exact fp64 GEMMs) plus stochastic acceptance of all {B} sequences at V={V}")
+    return flops_rep, times, desc
+
+
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        return max([d.get("num_threads", 1) for d in info] + [1]), \
+            ", ".join(sorted({f"{d.get('internal_api')} {d.get('version')}" for d in info})) or "unknown"
+    except Exception:
+        return os.cpu_count() or 1, "unknown"
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40, child=None):
+    """The oracle on the host cores: every core of this process (numpy's
+    BLAS pool) in-process, after the 1-thread child (start_1thread_oracle)
+    has finished, whose result is reported beside it.  `value` is the
+    all-cores figure in GEMM FLOPs per second of the median pass."""
+    child_out = None
+    if child is not None:
+        try:
+            child_out = child.communicate(timeout=300)
+        except Exception:
+            child.kill()
+            child_out = None
+    threads, blas = _blas_threads()
+    flops_rep, times, desc = _cpu_sample(wl, nfrac, min_seconds, max_reps)
+    med = float(np.median(times))
+    res = {"value": flops_rep / med / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"median of {len(times)} passes after one warm-up ({sum(times):.1f} s): {desc}",
+           "cpu_model": _cpu_model(), "blas": blas, "affinity_cpus": len(os.sched_getaffinity(0))}
+    try:
+        if child_out is None:
+            raise RuntimeError("no 1-thread child result")
+        out, err = child_out
+        if child.returncode != 0:
+            raise RuntimeError(err.strip().splitlines()[-1] if err.strip() else f"exit {child.returncode}")
+        f1, t1 = json.loads(out.strip().splitlines()[-1])
+        res["value_1thread"] = f1 / float(np.median(t1)) / 1e12
+        res["sample_1thread"] = f"median of {len(t1)} passes after one warm-up, same sample, 1 thread"
+    except Exception as e:       # the 1-thread figure is context; its absence is reported, not fatal
+        if child is not None and child.poll() is None:
+            child.kill()
+        res["value_1thread"] = None
+        res["sample_1thread"] = f"not measured: {str(e)[:120]}"
+    return res
+
+
+def start_1thread_oracle(nfrac=16):
+    """The 1-thread oracle pass as a child process, started before this
+    process touches the GPU; its thread variables are set before numpy is
+    imported.  cpu_baseline collects its result."""
+    import subprocess
+    env = dict(os.environ, OMP_NUM_THREADS="1", OPENBLAS_NUM_THREADS="1", MKL_NUM_THREADS="1")
+    code = ("import json, sys; sys.path.insert(0, %r); import bench, workloads as wl; "
+            "f, t, _ = bench._cpu_sample(wl, %d, 0.0, 3); print(json.dumps([f, t]))" % (ROOT, nfrac))
+    return subprocess.Popen([sys.executable, "-c", code], env=env, cwd=ROOT, stdout=subprocess.PIPE,
+                            stderr=subprocess.PIPE, text=True)
 
 
 COPY_BYTES = 256 << 20
@@ -670,11 +733,16 @@ def main(argv=None):
               f"MI355X; a sharded version is a design note, not a measured configuration.", file=sys.stderr)
         return 2
 
+    # the 1-thread oracle runs in a child started before this process touches the GPU
+    child = start_1thread_oracle() if (not args.no_cpu_baseline and args.profile is None) else None
+
     import torch
     import paper_2606_18502_amd as p
     import workloads as wl
 
     if not torch.cuda.is_available():
+        if child is not None:
+            child.kill()
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     p.load_library()
@@ -803,7 +871,7 @@ def main(argv=None):
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
-        res["cpu_baseline"] = cpu_baseline(wl)
+        res["cpu_baseline"] = cpu_baseline(wl, child=child)
     print(json.dumps(res), flush=True)
     return 0
 
