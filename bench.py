@@ -651,6 +651,29 @@ def start_1thread_oracle(nfrac=16):
                             stderr=subprocess.PIPE, text=True)
 
 
+def read_sclk():
+    """The GPU core clock from the driver's DPM table in sysfs: the listed
+    levels (MHz) and the level marked current, or None where not readable."""
+    import glob
+    for f in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            lines = open(f).read().splitlines()
+        except OSError:
+            continue
+        levels, current = [], None
+        for ln in lines:
+            parts = ln.replace("*", " ").split()
+            mhz = [int(x[:-3]) for x in parts if x.lower().endswith("mhz") and x[:-3].isdigit()]
+            if not mhz:
+                continue
+            if not ln.startswith("S:"):
+                levels.append(mhz[0])
+            if "*" in ln:
+                current = mhz[0]
+        return {"levels_mhz": levels, "current_mhz": current}
+    return None
+
+
 COPY_BYTES = 256 << 20
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_gate_up_M320_N28672_K4096_traffic.md")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2606_18502_amd", "csrc", "gemm.hip")
@@ -792,6 +815,7 @@ def main(argv=None):
     for i in range(args.steps):
         graphs[i % args.copies].replay()
     e1.record()
+    clock = read_sclk()                 # read while the replays run on the GPU
     torch.cuda.synchronize()
     ms_step_graph = e0.elapsed_time(e1) / args.steps
 
@@ -852,6 +876,7 @@ def main(argv=None):
             "verified_tokens_per_s_accept": round(tokens / (acc_us * 1e-6), 0),
             "verified_tokens_per_s_step": round(tokens / (ms_step * 1e-3), 0),
             "ms_per_step_graph": round(ms_step_graph, 4),
+            "gpu_sclk": clock,
             # projection, not a measurement: 40 layers (target 32 + drafter 8) of these linears and
             # quantizes plus one acceptance; attention, norms and the LM head are not included
             "projected_tokens_per_s_40_layers": round(
