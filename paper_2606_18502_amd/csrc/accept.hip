@@ -766,7 +766,7 @@ __device__ __forceinline__ void tree_outputs(const AcceptArgs& a, int b, const i
 // Greedy walk (one block per sequence): the argmax of every row from its
 // slice statistics, then from the root the first child whose token is the
 // current row's argmax, until no child matches; that argmax is emitted.
-__global__ __launch_bounds__(256) void tree_greedy_kernel(AcceptArgs a) {
+__global__ __launch_bounds__(1024) void tree_greedy_kernel(AcceptArgs a) {
     __shared__ int g[kMaxTree + 1];
     __shared__ int s_par[kMaxTree], s_x[kMaxTree], s_path[kMaxTree];
     __shared__ int s_depth, s_tok;
@@ -777,7 +777,10 @@ __global__ __launch_bounds__(256) void tree_greedy_kernel(AcceptArgs a) {
         s_par[t] = a.parent[(int64_t)b * N + t];
         s_x[t] = a.x[(int64_t)b * N + t];
     }
-    for (int r = wv; r <= N; r += 4) {
+    // rows over all waves (16): each merge is one dependent round trip, so
+    // the N+1 <= 65 rows take at most 5 in a row
+    const int nw = (int)(blockDim.x >> 6);
+    for (int r = wv; r <= N; r += nw) {
         const int bi = merged_argmax(a, b, r, lane);
         if (lane == 0) g[r] = bi;
     }
@@ -841,11 +844,30 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
         if (ok) zx = bf16_to_f32(a.zt[((int64_t)b * (N + 1) + par + 1) * a.V + xv]);
     }
     if (t <= N) s_u[t] = a.u[(int64_t)b * (N + 1) + t];
-    for (int r = wv; r <= N; r += kWavesPerBlock) {
+    // wave wv merges rows wv, wv+4, ...: the first entry of every one of its
+    // rows is loaded before any is merged (one round trip for all of them),
+    // then each lane merges its entries in index order
+    constexpr int kTreeRowsPerWave = (kMaxTree + 1 + kWavesPerBlock - 1) / kWavesPerBlock;
+    float2 first[kTreeRowsPerWave];
+#pragma unroll
+    for (int i = 0; i < kTreeRowsPerWave; ++i) {
+        const int r = wv + i * kWavesPerBlock;
+        first[i] = make_float2(-INFINITY, 0.0f);
+        if (r <= N) {
+            uint32_t nst;
+            const float2* st = row_stats(a, b, r, nst);
+            if ((uint32_t)lane < nst) first[i] = st[lane];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kTreeRowsPerWave; ++i) {
+        const int r = wv + i * kWavesPerBlock;
+        if (r > N) break;
         uint32_t nst;
         const float2* st = row_stats(a, b, r, nst);
         float m = -INFINITY, z = 0.0f;
-        for (int64_t q0 = lane; q0 < nst; q0 += 8 * kWave) {
+        merge_ms(m, z, first[i].x, first[i].y);
+        for (int64_t q0 = lane + kWave; q0 < nst; q0 += 8 * kWave) {
             float2 v[8];
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
@@ -1097,7 +1119,7 @@ hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int
         else hipLaunchKernelGGL(greedy_partial_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(tree_greedy_kernel, dim3((unsigned)B), dim3(256), 0, stream, a);
+        hipLaunchKernelGGL(tree_greedy_kernel, dim3((unsigned)B), dim3(1024), 0, stream, a);
         return hipGetLastError();
     }
     a.c2 = (float)(1.4426950408889634 / (double)temperature);
