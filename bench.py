@@ -604,6 +604,37 @@ def _cpu_model():
     return "unknown"
 
 
+def greedy_accept_part(torch, p, step, logits, reps=10, per_graph=10):
+    """Greedy acceptance (temperature 0, drafts matched against the target
+    argmax) over the same C4 target logits, as HIP-graph replays; returns the
+    mean us per call and GB/s over the target logits read once."""
+    zt, zd, x, _ = logits[0]
+    out = torch.empty_like(step.out)
+    num = torch.empty_like(step.num)
+    xg = torch.argmax(zd.float(), dim=-1).to(torch.int32)       # argmax drafts from the draft logits
+    call = lambda: p.verify_accept(zt, None, xg, None, 0.0, workspace=step.aws, out_tokens=out, num_accepted=num)
+    call()
+    torch.cuda.synchronize()
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gr):
+        for _ in range(per_graph):
+            call()
+    gr.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        gr.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * per_graph)
+    nbytes = 2.0 * zt.numel()
+    return {"us": round(us, 2), "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "pct_hbm_peak": round(100 * nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),
+            "mean_accepted_plus_one": round(float(num.float().mean().item()) + 1.0, 3),
+            "workload": "greedy acceptance, C4 target logits [64, 5, 128256] bf16, argmax drafts"}
+
+
 def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40, child=None):
     """The oracle on the host cores: every core of this process (numpy's
     BLAS pool) in-process, after the 1-thread child (start_1thread_oracle)
@@ -826,6 +857,7 @@ def main(argv=None):
     more = draft_and_kv_parts(torch, p, wl, step)
     quant = quantize_parts(torch, p, wl, step)
     others = other_configs(torch, p, wl)
+    greedy = greedy_accept_part(torch, p, step, logits)
     log(f"C2 layer GEMMs {others['C2']['layer_gemm_us']} us ({others['C2']['layer_pct_hbm_peak']}% of HBM peak); "
         f"C5 up {others['C5']['up_pct_mfma_peak']}%, down {others['C5']['down_pct_mfma_peak']}% of FP8 peak")
     log(f"quantize C5 4096x14336 per-token {quant['h_4096x14336_per_token_us']} us "
@@ -869,6 +901,7 @@ def main(argv=None):
             "drafter_and_kv_cache": more,
             "quantize": quant,
             "other_configs": others,
+            "accept_greedy": greedy,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),

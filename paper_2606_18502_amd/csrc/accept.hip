@@ -220,12 +220,14 @@ __global__ __launch_bounds__(kAThreads) void greedy_partial_kernel(AcceptArgs a)
     });
 }
 
-__global__ __launch_bounds__(256) void greedy_final_kernel(AcceptArgs a) {
+__global__ __launch_bounds__(1024) void greedy_final_kernel(AcceptArgs a) {
     __shared__ int g[17];
     const int b = blockIdx.x;
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-    // wave wv merges positions wv, wv+4, ...; lanes stride over the slices
-    for (int pos = wv; pos <= a.k; pos += 4) {
+    // wave wv merges positions wv, wv+16, ... (one round for k < 16); lanes
+    // stride over the slices
+    const int nw = (int)(blockDim.x >> 6);
+    for (int pos = wv; pos <= a.k; pos += nw) {
         uint32_t nst;
         const float2* st = row_stats(a, b, pos, nst);
         float bv = -INFINITY;
@@ -1071,7 +1073,7 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
-        hipLaunchKernelGGL(greedy_final_kernel, dim3((unsigned)B), dim3(256), 0, stream, a);
+        hipLaunchKernelGGL(greedy_final_kernel, dim3((unsigned)B), dim3(1024), 0, stream, a);
         return hipGetLastError();
     }
     a.R = (uint32_t)((k + 1) + (zd ? k : 0));
