@@ -682,26 +682,31 @@ def start_1thread_oracle(nfrac=16):
                             stderr=subprocess.PIPE, text=True)
 
 
+def parse_dpm(text):
+    """Levels (MHz, the listed DPM states) and the state marked current ('*')
+    of a pp_dpm_sclk table; a sleep state 'S:' counts as current only."""
+    levels, current = [], None
+    for ln in text.splitlines():
+        parts = ln.replace("*", " ").split()
+        mhz = [int(x[:-3]) for x in parts if x.lower().endswith("mhz") and x[:-3].isdigit()]
+        if not mhz:
+            continue
+        if not ln.startswith("S:"):
+            levels.append(mhz[0])
+        if "*" in ln:
+            current = mhz[0]
+    return {"levels_mhz": levels, "current_mhz": current}
+
+
 def read_sclk():
-    """The GPU core clock from the driver's DPM table in sysfs: the listed
-    levels (MHz) and the level marked current, or None where not readable."""
+    """The GPU core clock from the driver's DPM table in sysfs (parse_dpm), or
+    None where no table is readable."""
     import glob
     for f in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
         try:
-            lines = open(f).read().splitlines()
+            return parse_dpm(open(f).read())
         except OSError:
             continue
-        levels, current = [], None
-        for ln in lines:
-            parts = ln.replace("*", " ").split()
-            mhz = [int(x[:-3]) for x in parts if x.lower().endswith("mhz") and x[:-3].isdigit()]
-            if not mhz:
-                continue
-            if not ln.startswith("S:"):
-                levels.append(mhz[0])
-            if "*" in ln:
-                current = mhz[0]
-        return {"levels_mhz": levels, "current_mhz": current}
     return None
 
 
