@@ -112,6 +112,12 @@ def test_silu_mul_intermediate_and_fused_codes():
     np.testing.assert_array_equal(sg[same], s_o[same])
     step = np.abs(qg.astype(np.int32) - q_o.astype(np.int32))   # same sign: adjacent codes differ by 1
     assert np.max(step[~same], initial=0) <= 1
+    assert np.mean(step != 0) <= 1e-4
+    # given the GPU's own bf16 intermediate h, the fused codes and scales are the
+    # oracle's quantization of h, bit for bit
+    q_h, s_h = oq.quantize_rows(h_g)
+    np.testing.assert_array_equal(qg, q_h)
+    np.testing.assert_array_equal(sg, s_h)
 
 
 def test_per_tensor_from_calibration_matches_row_scales():
