@@ -567,26 +567,39 @@ def _cpu_sample(wl, nfrac, min_seconds, max_reps):
     u = wl.philox_uniforms((B, k + 1), seed=cfg4["uniform_seed"])
     flops_rep = sum(2.0 * M * (N // nfrac) * K for _, N, K in cfg3["linears"])
 
+    per_fn = {"quantize": [], "gemm": [], "accept": []}
+
     def one_pass():
+        tq = tg = 0.0
         for name, N, K in cfg3["linears"]:
+            t1 = time.perf_counter()
             if name == "down":
                 a, sa, _ = oq.quantize_silu_mul_rows(xs[name])
             else:
                 a, sa = oq.quantize_rows(xs[name])
+            t2 = time.perf_counter()
             w, sw = wq[name]
             og.gemm(a, sa, w, sw)
+            tq += t2 - t1
+            tg += time.perf_counter() - t2
+        t3 = time.perf_counter()
         oa.accept_stochastic(zt, zd, x, u, T)
+        return tq, tg, time.perf_counter() - t3
 
     one_pass()                                                      # warm-up
     times = []
     t0 = time.perf_counter()
     while len(times) < 3 or (time.perf_counter() - t0 < min_seconds and len(times) < max_reps):
         t1 = time.perf_counter()
-        one_pass()
+        tq, tg, ta = one_pass()
         times.append(time.perf_counter() - t1)
+        per_fn["quantize"].append(tq)
+        per_fn["gemm"].append(tg)
+        per_fn["accept"].append(ta)
     desc = (f"the 4 layer linears at M={M} on every {nfrac}th output channel (full K; per-token and "
             f"SiLU-gated quantize, exact fp64 GEMMs) plus stochastic acceptance of all {B} sequences at V={V}")
-    return flops_rep, times, desc
+    medians = {k: round(float(np.median(v)), 4) for k, v in per_fn.items()}
+    return flops_rep, times, desc, medians
 
 
 def _blas_threads():
@@ -653,10 +666,11 @@ def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40, child=None):
             child.kill()
             child_out = None
     threads, blas = _blas_threads()
-    flops_rep, times, desc = _cpu_sample(wl, nfrac, min_seconds, max_reps)
+    flops_rep, times, desc, medians = _cpu_sample(wl, nfrac, min_seconds, max_reps)
     med = float(np.median(times))
     res = {"value": flops_rep / med / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
            "sample": f"median of {len(times)} passes after one warm-up ({sum(times):.1f} s): {desc}",
+           "per_function_median_s": medians,
            "cpu_model": _cpu_model(), "blas": blas, "affinity_cpus": len(os.sched_getaffinity(0))}
     try:
         if child_out is None:
@@ -664,8 +678,9 @@ def cpu_baseline(wl, nfrac=16, min_seconds=10.0, max_reps=40, child=None):
         out, err = child_out
         if child.returncode != 0:
             raise RuntimeError(err.strip().splitlines()[-1] if err.strip() else f"exit {child.returncode}")
-        f1, t1 = json.loads(out.strip().splitlines()[-1])
+        f1, t1, m1 = json.loads(out.strip().splitlines()[-1])
         res["value_1thread"] = f1 / float(np.median(t1)) / 1e12
+        res["per_function_median_s_1thread"] = m1
         res["sample_1thread"] = f"median of {len(t1)} passes after one warm-up, same sample, 1 thread"
     except Exception as e:       # the 1-thread figure is context; its absence is reported, not fatal
         if child is not None and child.poll() is None:
@@ -682,7 +697,7 @@ def start_1thread_oracle(nfrac=16):
     import subprocess
     env = dict(os.environ, OMP_NUM_THREADS="1", OPENBLAS_NUM_THREADS="1", MKL_NUM_THREADS="1")
     code = ("import json, sys; sys.path.insert(0, %r); import bench, workloads as wl; "
-            "f, t, _ = bench._cpu_sample(wl, %d, 0.0, 3); print(json.dumps([f, t]))" % (ROOT, nfrac))
+            "f, t, _, m = bench._cpu_sample(wl, %d, 0.0, 3); print(json.dumps([f, t, m]))" % (ROOT, nfrac))
     return subprocess.Popen([sys.executable, "-c", code], env=env, cwd=ROOT, stdout=subprocess.PIPE,
                             stderr=subprocess.PIPE, text=True)
 
