@@ -150,3 +150,19 @@ def clip_rate(x_bits: np.ndarray, lo: float, hi: float) -> float:
     if x.size == 0:
         return 0.0
     return float(np.mean((x < np.float32(lo)) | (x > np.float32(hi))))
+
+
+def clip_count_static(x_bits: np.ndarray, scale: float) -> int:
+    """Number of values the static per-tensor quantizer saturates: those with
+    |fl32(x * fl32(1/s))| > 448, the largest E4M3 magnitude.
+
+    This is the paper's activation clip rate (§5 FP8 Calibration Performance:
+    test activations outside the calibrated per-tensor bounds) read through
+    the quantizer itself: with s = fl32(amax/448) from min-max calibration, a
+    value clips exactly when its scaled magnitude leaves the E4M3 range, i.e.
+    when |x| exceeds the calibrated amax up to the rounding of s and 1/s.
+    """
+    x = bf16_to_f32(x_bits)
+    inv = reciprocal(np.array([scale], np.float32))[0]
+    y = (x * inv).astype(np.float32)
+    return int(np.count_nonzero(np.abs(y) > np.float32(448.0)))

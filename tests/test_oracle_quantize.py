@@ -125,3 +125,23 @@ def test_clip_rate_definition():
     assert (lo, hi) == (-2.0, 3.0)
     test = wl.bf16_bits_from_f32(np.array([[-2.5, -2.0, 0.0, 3.0, 3.5, 1.0, 10.0, -1.0]], np.float32))
     assert oq.clip_rate(test, lo, hi) == 3 / 8
+
+
+def test_clip_count_static_against_the_calibrated_range():
+    """A value clips iff it lies beyond the calibrated amax (up to the rounding
+    of s and 1/s); the calibration rows themselves never clip; every clipped
+    value encodes to +-448."""
+    cal = _rows(7, M=32)
+    s = oq.calibrate_per_tensor([cal])
+    assert oq.clip_count_static(cal, s) == 0
+    amax = float(np.max(np.abs(oq.bf16_to_f32(cal))))
+    vals = np.array([0.0, amax * 0.5, -amax * 0.99, amax * 1.02, -amax * 1.5, amax * 4.0, -amax * 1.02], np.float32)
+    bits = wl.bf16_bits_from_f32(vals)[None, :]
+    x = oq.bf16_to_f32(bits)[0]
+    expect = int(np.count_nonzero(np.abs(x) > amax * (1 + 2.0 ** -8)))
+    assert oq.clip_count_static(bits, s) == expect == 4
+    q = oq.quantize_per_tensor(bits, s)
+    clipped = np.abs(x) > amax * (1 + 2.0 ** -8)
+    assert np.all((q[0][clipped] & 0x7F) == 0x7E)
+    # halving the scale doubles the range needed: values above amax/2 now clip
+    assert oq.clip_count_static(bits, np.float32(s / 2)) == int(np.count_nonzero(np.abs(x) > amax / 2 * (1 + 2.0 ** -8)))
