@@ -120,6 +120,31 @@ spec_status spec_silu_mul_bf16(const void* x, int64_t rows, int64_t cols, int64_
                                void* h, int64_t ld_h, void* stream);
 
 /*
+ * spec_fp8_clip_count -- how many values a static per-tensor scale clips.
+ *
+ * The paper judges a static calibration by its activation clip rate: the share
+ * of test-time activations outside the per-tensor range set during
+ * calibration (section 5, FP8 Calibration Performance).  Read through the
+ * quantizer, a value clips when its scaled magnitude leaves the E4M3 range:
+ *
+ *   count += #{ (r, c) : |fl32(x[r,c] * fl32(1 / scale[0]))| > 448 }
+ *
+ * which for a scale from SPEC_SCALE_CALIBRATE (s = fl32(amax/448)) is the set
+ * of values beyond the calibrated amax, up to the rounding of s and 1/s.  The
+ * count is exact (no floating-point summation).
+ *
+ * x      bf16 [rows, ld_x], cols <= ld_x.
+ * scale  fp32 [1], finite and > 0 (read).
+ * count  uint64 [1], accumulated: the caller sets it (usually to 0) before the
+ *        first call; calls on one counter add up.
+ * Requirements: rows >= 0 (0 is a no-op), cols > 0 (SPEC_ERR_SHAPE); cols % 8 == 0
+ * (SPEC_ERR_UNSUPPORTED); x 16-byte aligned, ld_x % 8 == 0, scale 4-byte and
+ * count 8-byte aligned (SPEC_ERR_ALIGN).
+ */
+spec_status spec_fp8_clip_count(const void* x, int64_t rows, int64_t cols, int64_t ld_x, const float* scale,
+                                uint64_t* count, void* stream);
+
+/*
  * spec_fp8_kv_cache_write -- the verify step's new keys and values, quantized
  * to E4M3 and stored in a paged FP8 KV cache.
  *

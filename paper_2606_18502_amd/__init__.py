@@ -21,6 +21,7 @@ from ._lib import SpecError, load as load_library, LIB_PATH  # noqa: F401
 from .ops import (  # noqa: F401
     quantize,
     calibrate,
+    clip_count,
     silu_mul,
     kv_cache_write,
     gemm,

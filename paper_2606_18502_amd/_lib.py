@@ -17,7 +17,7 @@ SCALE_PER_ROW, SCALE_PER_TENSOR, SCALE_CALIBRATE = 0, 1, 2
 QIN_BF16, QIN_SILU_MUL_BF16 = 0, 1
 OUT_BF16, OUT_F32 = 0, 1
 
-EXPORTS = ("spec_fp8_quantize", "spec_silu_mul_bf16", "spec_fp8_kv_cache_write", "spec_fp8_gemm_workspace_bytes", "spec_fp8_gemm",
+EXPORTS = ("spec_fp8_quantize", "spec_silu_mul_bf16", "spec_fp8_kv_cache_write", "spec_fp8_clip_count", "spec_fp8_gemm_workspace_bytes", "spec_fp8_gemm",
            "spec_fp8_gemm_silu_mul", "spec_logit_stats_count", "spec_fp8_gemm_logit_stats",
            "spec_verify_accept_workspace_bytes", "spec_verify_accept", "spec_verify_accept_stats",
            "spec_verify_accept_tree_workspace_bytes", "spec_verify_accept_tree", "spec_tree_attention_mask",
@@ -48,6 +48,8 @@ def load() -> ctypes.CDLL:
     lib.spec_fp8_quantize.restype = i32
     lib.spec_silu_mul_bf16.argtypes = [vp, i64, i64, i64, vp, i64, vp]
     lib.spec_silu_mul_bf16.restype = i32
+    lib.spec_fp8_clip_count.argtypes = [vp, i64, i64, i64, vp, vp, vp]
+    lib.spec_fp8_clip_count.restype = i32
     lib.spec_fp8_kv_cache_write.argtypes = [vp, i64, vp, i64, vp, i64, i64, i64, i64, i32, vp, vp, vp, vp, vp]
     lib.spec_fp8_kv_cache_write.restype = i32
     lib.spec_fp8_gemm_workspace_bytes.argtypes = [i64, i64, i64]

@@ -45,6 +45,14 @@ spec_status spec_silu_mul_bf16(const void* x, int64_t rows, int64_t cols, int64_
                                              reinterpret_cast<uint16_t*>(h), ld_h, as_stream(stream)));
 }
 
+spec_status spec_fp8_clip_count(const void* x, int64_t rows, int64_t cols, int64_t ld_x, const float* scale,
+                               uint64_t* count, void* stream) {
+    const spec_status st = specfp8::check_clip_count(x, rows, cols, ld_x, scale, count);
+    if (st != SPEC_OK || rows == 0) return st;
+    return from_hip(specfp8::launch_clip_count(reinterpret_cast<const uint16_t*>(x), rows, cols, ld_x, scale,
+                                               reinterpret_cast<unsigned long long*>(count), as_stream(stream)));
+}
+
 spec_status spec_fp8_kv_cache_write(const void* k, int64_t ld_k, const void* v, int64_t ld_v,
                                     const int64_t* slot_mapping, int64_t T, int64_t H, int64_t D,
                                     int64_t num_slots, spec_scale_mode mode, float* k_scale, float* v_scale,
@@ -208,6 +216,6 @@ const char* spec_status_string(spec_status s) {
 
 int spec_last_hip_error(void) { return g_last_hip_error; }
 
-int spec_version(void) { return 500; }
+int spec_version(void) { return 510; }
 
 }  // extern "C"

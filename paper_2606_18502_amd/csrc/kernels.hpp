@@ -12,6 +12,9 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t cols, int64_
                            int mode, float* scales, uint8_t* q, int64_t ld_q, hipStream_t stream);
 hipError_t launch_silu_mul(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x,
                            uint16_t* h, int64_t ld_h, hipStream_t stream);
+// count += number of x values with |fl32(x * fl32(1/scale[0]))| > 448
+hipError_t launch_clip_count(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x, const float* scale,
+                             unsigned long long* count, hipStream_t stream);
 
 // ---- kvcache.hip
 // Keys and values of T new tokens ([T][ld] bf16, H heads of D values each) to

@@ -151,6 +151,40 @@ __global__ __launch_bounds__(kQThreads) void silu_mul_bf16_kernel(
     }
 }
 
+// Values the static per-tensor quantizer saturates, |fl32(x * fl32(1/s))| >
+// 448 (the calibration clip rate of a test batch): grid-stride over 8-value
+// chunks read with 16-byte loads, a wave then block sum, one 64-bit atomic
+// add per block into the caller's counter.
+__global__ __launch_bounds__(kQThreads) void clip_count_kernel(const uint16_t* __restrict__ x, int64_t rows,
+                                                               int64_t cols, int64_t ld_x,
+                                                               const float* __restrict__ scale,
+                                                               unsigned long long* __restrict__ count) {
+    __shared__ unsigned int red[kQThreads / 64];
+    const float inv = (float)(1.0 / (double)scale[0]);
+    const int64_t nch = cols / 8;
+    const int64_t total = rows * nch;
+    unsigned int c = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = i / nch;
+        const int64_t ch = i - r * nch;
+        const uint4 p = *reinterpret_cast<const uint4*>(x + r * ld_x + ch * 8);
+        float v[8];
+        unpack8(p, v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) c += fabsf(v[e] * inv) > 448.0f ? 1u : 0u;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long sum = 0;
+        for (int w = 0; w < kQThreads / 64; ++w) sum += red[w];
+        if (sum) atomicAdd(count, sum);
+    }
+}
+
 template <int IN_KIND, int MODE>
 hipError_t launch_quantize_t(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x,
                              float* scales, uint8_t* q, int64_t ld_q, hipStream_t stream) {
@@ -200,6 +234,16 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t cols, int64_
     if (in_kind == 1 && mode == 2)
         return launch_quantize_t<1, 2>(x, rows, cols, ld_x, scales, q, ld_q, stream);
     return launch_quantize_t<1, 1>(x, rows, cols, ld_x, scales, q, ld_q, stream);
+}
+
+hipError_t launch_clip_count(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x, const float* scale,
+                             unsigned long long* count, hipStream_t stream) {
+    const int64_t total = rows * (cols / 8);
+    int64_t blocks = (total + kQThreads - 1) / kQThreads;
+    if (blocks > 2048) blocks = 2048;           // 8 workgroups per compute unit, grid-stride beyond
+    hipLaunchKernelGGL(clip_count_kernel, dim3((unsigned)blocks), dim3(kQThreads), 0, stream, x, rows, cols, ld_x,
+                       scale, count);
+    return hipGetLastError();
 }
 
 hipError_t launch_silu_mul(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld_x,

@@ -80,6 +80,19 @@ spec_status check_tree_mask(const int32_t* parents, int64_t B, int64_t N, const 
     return SPEC_OK;
 }
 
+spec_status check_clip_count(const void* x, int64_t rows, int64_t cols, int64_t ld_x, const float* scale,
+                             const void* count) {
+    if (rows < 0 || cols <= 0 || ld_x < cols) return SPEC_ERR_SHAPE;
+    if (cols % 8 != 0) return SPEC_ERR_UNSUPPORTED;
+    if (rows > INT64_MAX / cols) return SPEC_ERR_UNSUPPORTED;
+    if (rows == 0) return SPEC_OK;
+    if (!x || !scale || !count) return SPEC_ERR_NULL;
+    if (ld_x % 8 != 0 || !aligned16(x)) return SPEC_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(scale) & 3u) != 0 || (reinterpret_cast<uintptr_t>(count) & 7u) != 0)
+        return SPEC_ERR_ALIGN;
+    return SPEC_OK;
+}
+
 spec_status check_gemm(const void* a, int64_t lda, const float* a_scale, int a_mode, const void* w,
                        int64_t ldw, const float* w_scale, int w_mode, int64_t M, int64_t N, int64_t K,
                        const void* y, int64_t ldy, int out_dtype) {

@@ -14,6 +14,8 @@ spec_status check_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld
                            const float* scales, const void* q, int64_t ld_q);
 spec_status check_silu_mul(const void* x, int64_t rows, int64_t cols, int64_t ld_x, const void* h,
                            int64_t ld_h);
+spec_status check_clip_count(const void* x, int64_t rows, int64_t cols, int64_t ld_x, const float* scale,
+                             const void* count);
 spec_status check_gemm(const void* a, int64_t lda, const float* a_scale, int a_mode, const void* w,
                        int64_t ldw, const float* w_scale, int w_mode, int64_t M, int64_t N, int64_t K,
                        const void* y, int64_t ldy, int out_dtype);

@@ -99,6 +99,24 @@ def silu_mul(x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tenso
     return out
 
 
+def clip_count(x: torch.Tensor, scale: torch.Tensor, count: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Values of bf16 rows x that the static per-tensor scale clips (spec_fp8_clip_count):
+    |fl32(x * fl32(1/scale))| > 448.  Accumulates into `count` (int64 [1]
+    holding the uint64 count; a new zeroed counter if None) and returns it."""
+    lib = _lib.load()
+    _dev(x, torch.bfloat16, "x")
+    _dev(scale, torch.float32, "scale")
+    if scale.numel() != 1:
+        raise ValueError("scale must hold one fp32 value")
+    if count is None:
+        count = torch.zeros(1, dtype=torch.int64, device=x.device)
+    _dev(count, torch.int64, "count")
+    rows, cols = x.shape
+    check("spec_fp8_clip_count", lib.spec_fp8_clip_count(x.data_ptr(), rows, cols, _rowmajor(x, "x"),
+                                                         scale.data_ptr(), count.data_ptr(), _stream()))
+    return count
+
+
 def kv_cache_write(k: torch.Tensor, v: torch.Tensor, slot_mapping: torch.Tensor, k_cache: torch.Tensor,
                    v_cache: torch.Tensor, k_scale: torch.Tensor, v_scale: torch.Tensor,
                    per_tensor: bool = False) -> None:

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.spec_version() == 500
+    assert lib.spec_version() == 510
     for s in range(9):
         assert lib.spec_status_string(s)
     assert lib.spec_status_string(99) == b"unknown status"
@@ -124,6 +124,22 @@ def test_tree_mask_validation(lib):
     assert f(A16, 4, 5, A16 + 4, A16, None) == ALIGN
     assert f(A16, 4, 5, A16, A16 + 2, None) == ALIGN
     assert f(None, 0, 5, None, None, None) == OK
+
+
+def test_clip_count_validation(lib):
+    f = lib.spec_fp8_clip_count
+    assert f(A16, -1, 64, 64, A16, A16, None) == SHAPE
+    assert f(A16, 4, 0, 64, A16, A16, None) == SHAPE
+    assert f(A16, 4, 64, 32, A16, A16, None) == SHAPE
+    assert f(A16, 4, 60, 64, A16, A16, None) == UNSUP
+    assert f(None, 4, 64, 64, A16, A16, None) == NULL
+    assert f(A16, 4, 64, 64, None, A16, None) == NULL
+    assert f(A16, 4, 64, 64, A16, None, None) == NULL
+    assert f(A1, 4, 64, 64, A16, A16, None) == ALIGN
+    assert f(A16, 4, 64, 68, A16, A16, None) == ALIGN
+    assert f(A16, 4, 64, 64, A16 + 2, A16, None) == ALIGN
+    assert f(A16, 4, 64, 64, A16, A16 + 4, None) == ALIGN
+    assert f(None, 0, 64, 64, None, None, None) == OK
 
 
 def test_silu_mul_validation(lib):

@@ -20,5 +20,6 @@ from .gen import (  # noqa: F401
     tree_shape,
     tree_tokens_topk,
     paged_slot_mapping,
+    calibration_sets,
 )
 from .configs import CONFIGS, C4_CORRELATION, TREE25  # noqa: F401

@@ -61,6 +61,13 @@ CONFIGS = {
         B=64, k=4, V=VOCAB, logit_std=3.0, rank=8, temperature=0.7,
         seed=7, draft_seed=8, uniform_seed=7,
     ),
+    "CALSTUDY": dict(
+        desc="static per-tensor calibration study: clip rate of an 8192-token in-domain-like test set "
+             "against scales calibrated on 32..2048 tokens of a public-like, an in-domain-like and a "
+             "mixed synthetic set (hidden size 4096)",
+        K=HIDDEN, lengths=(32, 64, 128, 256, 512, 1024, 2048), test_tokens=8192,
+        public_outlier_frac=0.005, public_outlier_scale=30.0, indomain_df=3.0, seed=21,
+    ),
     "DRAFT": dict(
         desc="FP8 linears of the EAGLE-style drafter (the feature fc 8192->4096 plus one "
              "Llama-3.1-8B-shaped decoder layer, about 250M parameters) for one draft step of "

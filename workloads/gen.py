@@ -205,3 +205,16 @@ def paged_slot_mapping(B: int, new_tokens: int, ctx_lens, block_size: int, seed:
         pos = ctx[b] + np.arange(new_tokens)
         slots[b * new_tokens:(b + 1) * new_tokens] = page[pos // block_size] * block_size + pos % block_size
     return slots, int(need.sum()) * block_size
+
+
+def calibration_sets(L: int, K: int, seed: int, public_outlier_frac: float, public_outlier_scale: float,
+                     indomain_df: float):
+    """Calibration pools of L tokens for the calibration study: 'public'
+    (Gaussian activations with a few large outlier channels), 'in_domain'
+    (heavy-tailed Student-t activations, the test set's law) and 'mixed'
+    (the first half of each).  Returns {name: bf16 bits [L, K]}."""
+    pub = linear_activations(L, K, seed, public_outlier_frac, public_outlier_scale)
+    ind = student_t_activations(L, K, seed + 1, indomain_df)
+    h = L // 2
+    mix = np.concatenate([pub[:h], ind[:L - h]], axis=0)
+    return {"public": pub, "in_domain": ind, "mixed": mix}
