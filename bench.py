@@ -622,6 +622,54 @@ def _cpu_model():
     return "unknown"
 
 
+def calibration_study(torch, p, wl):
+    """The static-calibration study of the paper's FP8 Calibration Performance
+    section on synthetic stand-ins: per-tensor scales calibrated on the first
+    L tokens (L = 32 .. 2048) of a public-like, an in-domain-like and a mixed
+    set (workloads.calibration_sets), each judged by the clip rate of an
+    8192-token in-domain-like test set (spec_fp8_calibrate, then
+    spec_fp8_clip_count).  Returns clip rates per set and L, and the clip-count
+    kernel's time and GB/s on the test set."""
+    c = wl.CONFIGS["CALSTUDY"]
+    K, T = c["K"], c["test_tokens"]
+    test = wl.student_t_activations(T, K, c["seed"] + 100, c["indomain_df"])
+    dtest = torch.from_numpy(np.ascontiguousarray(test).view(np.int16)).view(torch.bfloat16).to("cuda")
+    rates = {}
+    for L in c["lengths"]:
+        sets = wl.calibration_sets(L, K, c["seed"], c["public_outlier_frac"], c["public_outlier_scale"],
+                                   c["indomain_df"])
+        for name, cal in sets.items():
+            run = torch.zeros(1, dtype=torch.float32, device="cuda")
+            p.calibrate(torch.from_numpy(np.ascontiguousarray(cal).view(np.int16)).view(torch.bfloat16).to("cuda"),
+                        run)
+            n = int(p.clip_count(dtest, run).item())
+            rates.setdefault(name, {})[str(L)] = n / float(T * K)
+    # the counting kernel on the test set (67 MB of bf16), graph replays
+    s1 = torch.ones(1, dtype=torch.float32, device="cuda")
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    p.clip_count(dtest, s1, count=cnt)
+    torch.cuda.synchronize()
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gr):
+        for _ in range(10):
+            p.clip_count(dtest, s1, count=cnt)
+    gr.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        gr.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / 50
+    nbytes = 2.0 * T * K
+    return {"clip_rate": rates, "clip_count_us": round(us, 2), "clip_count_gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "workload": f"clip rate of {T} in-domain-like test tokens x {K} (Student-t({c['indomain_df']:g})) "
+                        f"against per-tensor scales calibrated on L = {list(c['lengths'])} tokens of synthetic "
+                        f"public-like (Gaussian, {c['public_outlier_frac']:g} outlier channels x"
+                        f"{c['public_outlier_scale']:g}), in-domain-like and mixed (half each) sets"}
+
+
 def greedy_accept_part(torch, p, step, logits, reps=10, per_graph=10):
     """Greedy acceptance (temperature 0, drafts matched against the target
     argmax) over the same C4 target logits, as HIP-graph replays; returns the
@@ -883,6 +931,7 @@ def main(argv=None):
     quant = quantize_parts(torch, p, wl, step)
     others = other_configs(torch, p, wl)
     greedy = greedy_accept_part(torch, p, step, logits)
+    calib = calibration_study(torch, p, wl)
     log(f"C2 layer GEMMs {others['C2']['layer_gemm_us']} us ({others['C2']['layer_pct_hbm_peak']}% of HBM peak); "
         f"C5 up {others['C5']['up_pct_mfma_peak']}%, down {others['C5']['down_pct_mfma_peak']}% of FP8 peak")
     log(f"quantize C5 4096x14336 per-token {quant['h_4096x14336_per_token_us']} us "
@@ -928,6 +977,7 @@ def main(argv=None):
             "quantize": quant,
             "other_configs": others,
             "accept_greedy": greedy,
+            "calibration_study": calib,
             "accept_us": round(acc_us, 1),
             "accept_gbps": round(acc_bytes / (acc_us * 1e-6) / 1e9, 1),
             "accept_pct_hbm_peak": round(100 * acc_bytes / (acc_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),
