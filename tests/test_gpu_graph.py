@@ -176,3 +176,64 @@ def test_graph_replays_of_the_lm_head_and_tree_paths():
         got = snapshot()
         for i, (a, b) in enumerate(zip(got, ref)):
             assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), (rep, i)
+
+
+def test_graph_replays_of_kv_cache_tree_mask_and_clip_count():
+    """The FP8 KV-cache write, the tree attention masks and the clip count
+    (its counter cleared by a fill kernel inside the graph) replayed with new
+    inputs, each replay equal to eager calls on the same inputs."""
+    p = need_gpu()
+    T, H, D, S = 40, 8, 128, 96
+    N, B = 25, 16
+    dev = "cuda"
+    kx = torch.empty((T, H, D), dtype=torch.bfloat16, device=dev)
+    vx = torch.empty_like(kx)
+    slots = torch.empty((T,), dtype=torch.int64, device=dev)
+    kc = torch.zeros((S, H, D), dtype=torch.uint8, device=dev)
+    vc = torch.zeros_like(kc)
+    ks = torch.zeros((S, H), dtype=torch.float32, device=dev)
+    vs = torch.zeros_like(ks)
+    par = torch.empty((B, N), dtype=torch.int32, device=dev)
+    mask = torch.empty((B, N), dtype=torch.int64, device=dev)
+    depth = torch.empty((B, N), dtype=torch.int32, device=dev)
+    scale = torch.empty((1,), dtype=torch.float32, device=dev)
+    cnt = torch.zeros((1,), dtype=torch.int64, device=dev)
+
+    def load(seed):
+        rng = np.random.default_rng(seed)
+        kx.copy_(dev_bf16(wl.linear_activations(T, H * D, seed, 0.01, 20.0)).view(T, H, D))
+        vx.copy_(dev_bf16(wl.linear_activations(T, H * D, seed + 1)).view(T, H, D))
+        sl = rng.choice(S, T, replace=False).astype(np.int64)
+        sl[3] = -1
+        slots.copy_(torch.from_numpy(sl))
+        par.copy_(dev_i32(np.array([[int(rng.integers(-1, n)) if n else -1 for n in range(N)]
+                                    for _ in range(B)], np.int32)))
+        scale.copy_(dev_f32([0.02 + 0.01 * (seed % 3)]))
+
+    def run():
+        kc.zero_(); vc.zero_(); ks.zero_(); vs.zero_(); cnt.zero_()
+        p.kv_cache_write(kx, vx, slots, kc, vc, ks, vs)
+        p.tree_attention_mask(par, mask=mask, depth=depth)
+        p.clip_count(kx.view(T, H * D), scale, count=cnt)
+
+    def snap():
+        torch.cuda.synchronize()
+        return [t.clone() for t in (kc, vc, ks, vs, mask, depth, cnt)]
+
+    load(1)
+    run()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run()
+    for rep, seed in enumerate((5, 6, 6, 9)):
+        say(f"graph replay {rep} (inputs seed {seed})")
+        load(seed)
+        run()
+        ref = snap()
+        load(seed)
+        g.replay()
+        got = snap()
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b)
+        torch.cuda.synchronize()
