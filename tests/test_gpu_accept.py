@@ -262,3 +262,45 @@ def test_stochastic_largest_vocabulary():
         assert num[b] == (acc.index(False) if False in acc else k)
     _check_valid(out, num, x, V)
     _sample_position_ok(out, num, zt, zd, x, u, T)
+
+
+def test_million_trials_law_and_mean_acceptance():
+    """One target/draft logit set replicated over 9000 sequences (B (2k+1) <=
+    65535), 112 rounds of fresh drafts (sampled from q) and uniforms: about
+    10^6 verify trials at V = 256.  The first emitted token follows p_0 (chi-square), and the mean
+    number of accepted drafts matches the closed form
+    E[a] = sum_j prod_{i<j} beta_i, beta_i = sum_v min(p_i, q_i)
+    (within 6 standard errors)."""
+    p = need_gpu()
+    V, k, T, B, R = 256, 3, 1.0, 9000, 112
+    rng = np.random.default_rng(33)
+    zt1 = (rng.standard_normal((1, k + 1, V)) * 1.5).astype(np.float32)
+    zd1 = (zt1[:, :k] + 0.7 * rng.standard_normal((1, k, V))).astype(np.float32)
+    zt = wl.bf16_bits_from_f32(np.repeat(zt1, B, 0))
+    zd = wl.bf16_bits_from_f32(np.repeat(zd1, B, 0))
+    pp = [oa.softmax64(zt[0, i], T) for i in range(k + 1)]
+    qq = [oa.softmax64(zd[0, i], T) for i in range(k)]
+    e_a = oa.expected_accepted(pp[:k], qq)
+    dzt, dzd = dev_bf16(zt), dev_bf16(zd)
+    counts = np.zeros(V)
+    acc = []
+    for rep in range(R):
+        if rep % 16 == 0:
+            say(f"round {rep}")
+        x = wl.draft_tokens_sampled(zd, T, seed=1000 + rep)
+        u = wl.philox_uniforms((B, k + 1), seed=2000 + rep)
+        out, num = p.verify_accept(dzt, dzd, dev_i32(x), dev_f32(u), T)
+        counts += np.bincount(host(out)[:, 0], minlength=V)
+        acc.append(host(num).astype(np.float64))
+    n = counts.sum()
+    assert n == B * R
+    exp = pp[0] * n
+    keep = exp >= 5
+    chi2 = np.sum((counts[keep] - exp[keep]) ** 2 / exp[keep]) + \
+        (counts[~keep].sum() - exp[~keep].sum()) ** 2 / max(exp[~keep].sum(), 1e-9)
+    dof = keep.sum()
+    assert chi2 < dof + 6 * np.sqrt(2 * dof), (chi2, dof)
+    a = np.concatenate(acc)
+    se = a.std() / np.sqrt(a.size)
+    say(f"mean accepted {a.mean():.5f}, closed form {e_a:.5f}, standard error {se:.2e}; chi2 {chi2:.1f} (dof {dof})")
+    assert abs(a.mean() - e_a) < 6 * se + 1e-6
