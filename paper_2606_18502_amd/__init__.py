@@ -15,6 +15,19 @@ FP8 KV-cache write of the new tokens' keys and values (kv_cache_write).
 
 The computation lives in libspecfp8.so (HIP kernels behind the C ABI of
 include/spec_fp8.h); this package only marshals torch tensors into that ABI.
+
+A verify step, in outline (tensors on the GPU; shapes as in the docstrings):
+
+    import paper_2606_18502_amd as p
+    w_q, w_s = p.quantize(w_bf16)                 # once per weight: per-channel E4M3
+    a_q, a_s = p.quantize(x_bf16)                 # per token, at run time
+    y = p.gemm(a_q, a_s, w_q, w_s)                # bf16 [M, N], fp32 accumulation
+    h_q, h_s = p.quantize(y_gate_up, silu_mul=True)   # SiLU-gated input of the down projection
+    out, num = p.verify_accept(target_logits, draft_logits, draft_tokens, uniforms, 0.7)
+
+`out[b, :num[b] + 1]` are the tokens sequence b emits (accepted drafts, then
+the resampled or bonus token).  Static per-tensor scales: p.calibrate over
+calibration batches, then p.quantize(x, per_tensor_scale=s).
 """
 
 from ._lib import SpecError, load as load_library, LIB_PATH  # noqa: F401
