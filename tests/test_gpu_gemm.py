@@ -57,6 +57,7 @@ def _sample(n, count, seed):
     (300, 1000, 1024),                                     # 64x128 tile, ragged M and N, split-K
     (700, 400, 512), (1024, 1024, 1024),                   # 256-row tile
     (1300, 672, 256), (1777, 100, 128),                    # >= 8 M-tiles: grouped tile order, ragged group
+    (300, 60096, 256),                                     # 626 160x192 tiles (a wide N), ragged M
 ])
 def test_gemm_parity(M, N, K):
     p = need_gpu()
