@@ -843,6 +843,31 @@ def profile_gemm_c5(torch, p, wl):
     return 0
 
 
+def profile_accept_c4(torch, p, wl, reps=20):
+    """Kernels for a kernel-trace run of the acceptance alone: `reps` stochastic
+    (T = 0.7) and `reps` greedy acceptances of the C4 logits, back to back."""
+    c = wl.CONFIGS["C4"]
+    B, k, V, T = c["B"], c["k"], c["V"], c["temperature"]
+    zt, zd = wl.accept_logits(B, k, V, c["seed"], wl.C4_CORRELATION, scale=c["logit_std"], rank=c["rank"])
+    x = wl.draft_tokens_sampled(zd, T, seed=c["draft_seed"])
+    xg = wl.draft_tokens_greedy(zd)
+    u = wl.philox_uniforms((B, k + 1), seed=c["uniform_seed"])
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to("cuda")
+
+    dzt, dzd = dev(zt), dev(zd)
+    dx, dxg, du = (torch.from_numpy(a).to("cuda") for a in (x, xg, u))
+    ws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device="cuda")
+    for _ in range(reps):
+        p.verify_accept(dzt, dzd, dx, du, T, workspace=ws)
+    for _ in range(reps):
+        p.verify_accept(dzt, None, dxg, None, 0.0, workspace=ws)
+    torch.cuda.synchronize()
+    log("profile kernels done")
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -850,10 +875,11 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--copies", type=int, default=3, help="rotated copies of weights and logits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile", choices=["traffic", "gemm_c5"], default=None,
+    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "accept_c4"], default=None,
                     help="for hardware-counter runs: 'traffic' = a plain copy of 256 MiB (the counters' "
                          "calibration), then 3 launches of the gate|up GEMM; 'gemm_c5' = 3 launches of the "
-                         "M=4096 4096->14336 GEMM; then exit")
+                         "M=4096 4096->14336 GEMM; 'accept_c4' = 20 stochastic and 20 greedy acceptances of the "
+                         "C4 logits; then exit")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}): the verify path runs on one "
@@ -878,6 +904,8 @@ def main(argv=None):
         return profile_traffic(torch, p, wl)
     if args.profile == "gemm_c5":
         return profile_gemm_c5(torch, p, wl)
+    if args.profile == "accept_c4":
+        return profile_accept_c4(torch, p, wl)
     acts, weights, logits = build_inputs(torch, p, wl, args.copies)
     step = Step(torch, p, wl, acts)
     cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
