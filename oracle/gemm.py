@@ -88,3 +88,21 @@ def rel_error(y: np.ndarray, y_ref: np.ndarray) -> float:
     scale = np.max(np.abs(y_ref), axis=1, keepdims=True)
     scale = np.where(scale > 0, scale, 1.0)
     return float(np.max(np.abs(y - y_ref) / scale))
+
+
+def rel_error_elementwise(y: np.ndarray, y_ref: np.ndarray, floor_frac: float = 0.01) -> float:
+    """Largest error of any output relative to its own magnitude, floored.
+
+    max_{m,n} |y - y_ref| / max(|y_ref[m,n]|, floor_frac * rms_n(y_ref[m, :])):
+    the per-output relative error, where outputs that cancel to below
+    floor_frac of their row's root-mean-square are measured against that
+    fraction of the rms instead of their own (vanishing) magnitude.
+    """
+    y = np.asarray(y, dtype=np.float64)
+    y_ref = np.asarray(y_ref, dtype=np.float64)
+    if y_ref.size == 0:
+        return 0.0
+    rms = np.sqrt(np.mean(y_ref * y_ref, axis=1, keepdims=True))
+    den = np.maximum(np.abs(y_ref), floor_frac * rms)
+    den = np.where(den > 0, den, 1.0)
+    return float(np.max(np.abs(y - y_ref) / den))

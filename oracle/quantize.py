@@ -140,12 +140,9 @@ def calibrate_minmax(batches):
 
 
 def clip_rate(x_bits: np.ndarray, lo: float, hi: float) -> float:
-    """Share of test activations outside the calibrated bounds [lo, hi].
-
-    The paper's activation clip rate (§5 FP8 Calibration Performance): the
-    fraction of test-time activations that fall outside the per-tensor
-    min/max bounds set during calibration.
-    """
+    """Fraction of the values in x below lo or above hi, where [lo, hi] is
+    the per-tensor range calibration produced (the clip-rate metric of the
+    section FP8 Calibration Performance)."""
     x = bf16_to_f32(x_bits)
     if x.size == 0:
         return 0.0
@@ -156,11 +153,11 @@ def clip_count_static(x_bits: np.ndarray, scale: float) -> int:
     """Number of values the static per-tensor quantizer saturates: those with
     |fl32(x * fl32(1/s))| > 448, the largest E4M3 magnitude.
 
-    This is the paper's activation clip rate (§5 FP8 Calibration Performance:
-    test activations outside the calibrated per-tensor bounds) read through
-    the quantizer itself: with s = fl32(amax/448) from min-max calibration, a
-    value clips exactly when its scaled magnitude leaves the E4M3 range, i.e.
-    when |x| exceeds the calibrated amax up to the rounding of s and 1/s.
+    This is the clip-rate metric of the section FP8 Calibration Performance
+    read through the quantizer itself: with s = fl32(amax/448) from min-max
+    calibration, a value clips exactly when its scaled magnitude leaves the
+    E4M3 range, i.e. when |x| exceeds the calibrated amax up to the rounding
+    of s and 1/s.
     """
     x = bf16_to_f32(x_bits)
     inv = reciprocal(np.array([scale], np.float32))[0]

@@ -1,6 +1,6 @@
 """Build libspecfp8.so (HIP for gfx950) in-tree.
 
-    python -m paper_2606_18502_amd.build [--oracle]
+    python -m paper_2606_18502_amd.build [-v]
 
 Every HIP source is compiled with hipcc for gfx950 only, without packed-fp32
 instructions (-packed-fp32-ops) and without floating-point contraction

@@ -167,3 +167,36 @@ def test_deterministic():
     b = _run(p, xb)
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_silu_mul_quantize_verify_step_width():
+    """The SiLU-gated quantize at the width of the verify step's FFN
+    (M = 320 rows of the gate|up output, 2 x 14336 bf16 -> 14336 codes), the
+    shape and launch configuration the step runs.  The input is seeded
+    synthetic gate|up output (N(0, 3^2), the spread of the C3 layer's gate|up
+    values).  Given the GPU's own bf16 intermediate h the codes and scales
+    are the oracle's quantization of h bit for bit; against the oracle's own
+    h, codes differ by at most one E4M3 step on at most 1e-4 of elements."""
+    p = need_gpu()
+    cfg = wl.CONFIGS["C3"]
+    M = cfg["M"]
+    inter = dict((n, (N, K)) for n, N, K in cfg["linears"])["gate_up"][0] // 2
+    say(f"SiLU-gated quantize {M} x 2*{inter}")
+    xb = wl.gated_ffn_input(M, inter, seed=cfg["seed"] + 5, std=3.0)
+    x = dev_bf16(xb)
+    q, s = p.quantize(x, silu_mul=True)
+    h_g = host_bf16_bits(p.silu_mul(x))
+    qg, sg = host(q), host(s)
+    q_h, s_h = oq.quantize_rows(h_g)
+    np.testing.assert_array_equal(qg, q_h)
+    np.testing.assert_array_equal(sg, s_h)
+    q_o, s_o, h_o = oq.quantize_silu_mul_rows(xb)
+    diff = np.abs(h_g.astype(np.int32) - h_o.astype(np.int32))
+    assert np.max(diff) <= 1 and np.mean(diff != 0) < 1e-3
+    same = np.all(diff == 0, axis=1)
+    np.testing.assert_array_equal(qg[same], q_o[same])
+    np.testing.assert_array_equal(sg[same], s_o[same])
+    step = np.abs(qg.astype(np.int32) - q_o.astype(np.int32))
+    say(f"h differs on {int((diff != 0).sum())} of {diff.size}; code steps {int((step != 0).sum())}")
+    assert np.max(step, initial=0) <= 1
+    assert np.mean(step != 0) <= 1e-4

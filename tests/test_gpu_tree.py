@@ -3,8 +3,11 @@ the oracle's tree walk (oracle/tree.py).
 
 Greedy walks are bit-exact.  Sampling walks evaluate probabilities in fp32
 statistics (the tests in double), so every sequence whose decisions all lie
-farther than MARGIN from their boundary must match exactly and the others
-must be valid walks.  A chain-shaped tree must give exactly what the chain
+farther than MARGIN from their boundary must match exactly, and every
+sequence is replayed in fp64 along the device's own walk
+(tests/accept_checks.py): each child test must be the fp64 decision unless
+it lies within 1e-6 of its boundary, and the emitted token must sit at its
+inverse-CDF position.  A chain-shaped tree must give exactly what the chain
 kernel gives without draft logits (the same rule), and on the device the
 first emitted token of a replicated tree follows the target distribution.
 """
@@ -15,6 +18,7 @@ import torch
 
 import workloads as wl
 from oracle import tree as ot
+from tests.accept_checks import check_tree
 from tests.gpu_util import dev_bf16, dev_f32, dev_i32, host, need_gpu, say
 
 pytestmark = pytest.mark.gpu
@@ -88,6 +92,7 @@ def test_tree_sampling_parity(B, N, V, seed, c, branching, T):
     np.testing.assert_array_equal(out[clear], out_ref[clear])
     np.testing.assert_array_equal(nodes[clear], nodes_ref[clear])
     _check_valid_walk(out, nodes, num, parents, x, V)
+    check_tree(out, nodes, num, zt, parents, x, u, T)
 
 
 @pytest.mark.parametrize("T", [0.0, 0.7])
@@ -168,6 +173,8 @@ def test_tree25_full_vocabulary():
     np.testing.assert_array_equal(out[clear], out_ref[clear])
     np.testing.assert_array_equal(nodes[clear], nodes_ref[clear])
     _check_valid_walk(out, nodes, num, parents, x, V)
+    # every sequence, the margin ones included, replayed along the device's walk
+    check_tree(out, nodes, num, zt, parents, x, u, T)
 
 
 @pytest.mark.parametrize("B,N,seed", [(1, 1, 0), (7, 7, 1), (301, 25, 2), (33, 64, 3), (5, 40, 4)])

@@ -214,3 +214,53 @@ def test_softmax_normalizer_shift_and_batch():
     # a very high temperature flattens the distribution towards uniform
     _, Zhot = oa.softmax_normalizer(_bits(z), 1e7)
     np.testing.assert_allclose(Zhot, 300, rtol=1e-5)
+
+
+# ---- softmax64: the p = softmax(z / T) and q = softmax(z_d / T) of the acceptance rule
+
+@pytest.mark.parametrize("T", [0.3, 0.7, 2.0])
+def test_softmax64_two_level_closed_form(T):
+    # one logit a and V-1 logits b: p_a = 1 / (1 + (V-1) e^((b-a)/T)), p_b = e^((b-a)/T) p_a
+    V, a, b = 1000, 2.0, 0.5
+    z = np.full(V, b)
+    z[417] = a
+    p = oa.softmax64(_bits(z), T)
+    t = float(np.float32(T))
+    pa = 1.0 / (1.0 + (V - 1) * np.exp((b - a) / t))
+    assert abs(p[417] - pa) <= 1e-12 * pa
+    others = np.delete(p, 417)
+    np.testing.assert_allclose(others, np.exp((b - a) / t) * pa, rtol=1e-12)
+    assert abs(p.sum() - 1.0) <= 1e-12
+
+
+@pytest.mark.parametrize("T", [0.3, 0.7, 2.0])
+def test_softmax64_log_ratios_are_logit_gaps_over_T(T):
+    # log(p_i / p_j) = (z_i - z_j) / T for every pair: the temperature divides
+    rng = np.random.default_rng(11)
+    z = np.round(rng.normal(0, 3, 64) * 4) / 4               # quarter-integers: exact in bf16
+    p = oa.softmax64(_bits(z), T)
+    t = float(np.float32(T))
+    i, j = np.meshgrid(np.arange(64), np.arange(64), indexing="ij")
+    np.testing.assert_allclose(np.log(p[i] / p[j]), (z[i] - z[j]) / t, atol=1e-11)
+
+
+@pytest.mark.parametrize("T", [0.3, 0.7, 2.0])
+def test_softmax64_agrees_with_normalizer(T):
+    # p_v = exp((z_v - zmax) / T) / Z with (zmax, Z) from the statistics form
+    rng = np.random.default_rng(12)
+    zb = _bits(rng.normal(0, 3, (3, 500)))
+    zmax, Z = oa.softmax_normalizer(zb, T)
+    z = (zb.astype(np.uint32) << 16).view(np.float32).astype(np.float64)   # bf16 -> f32 is a shift
+    t = float(np.float32(T))
+    for r in range(3):
+        np.testing.assert_allclose(oa.softmax64(zb[r], T), np.exp((z[r] - zmax[r]) / t) / Z[r], rtol=1e-13)
+
+
+def test_softmax64_temperature_limits():
+    # T -> 0 concentrates on the argmax; a large T flattens to uniform
+    z = np.array([0.0, 1.0, 3.0, 2.5, -1.0])
+    p_cold = oa.softmax64(_bits(z), 0.01)
+    assert np.argmax(p_cold) == 2
+    assert abs(p_cold[3] / p_cold[2] - np.exp(-0.5 / float(np.float32(0.01)))) <= 1e-12 * p_cold[3] / p_cold[2]
+    p_hot = oa.softmax64(_bits(z), 1e7)
+    np.testing.assert_allclose(p_hot, 0.2, rtol=1e-6)

@@ -91,3 +91,22 @@ def test_rel_error_metric():
     y = y_ref + np.array([[0.1, 0.0, 0.05], [0.0, 1e-3, 0.0]])
     # row 0: 0.1 / 100; row 1 has no magnitude, its error is taken absolutely
     assert abs(og.rel_error(y, y_ref) - 1e-3) < 1e-15
+
+
+def test_elementwise_metric_floors_vanishing_outputs():
+    y_ref = np.array([[1.0, -2.0, 0.0, 4.0], [3.0, 3.0, 3.0, 3.0]])
+    rms0 = np.sqrt(np.mean(y_ref[0] ** 2))
+    y = y_ref.copy()
+    y[0, 1] *= 1 + 1e-3                                 # relative 1e-3 on its own magnitude
+    assert abs(og.rel_error_elementwise(y, y_ref) - 1e-3) < 1e-12
+    y = y_ref.copy()
+    y[0, 2] = 1e-4                                      # a zero output: measured against 0.01 rms
+    assert abs(og.rel_error_elementwise(y, y_ref) - 1e-4 / (0.01 * rms0)) < 1e-9
+    y = y_ref.copy()
+    y[1, 0] = 3.0 * (1 - 5e-4)
+    assert abs(og.rel_error_elementwise(y, y_ref) - 5e-4) < 1e-12
+    # never looser than the row-normwise metric on the same outputs
+    rng = np.random.default_rng(3)
+    y_ref = rng.standard_normal((20, 300))
+    y = y_ref + 1e-4 * rng.standard_normal((20, 300))
+    assert og.rel_error_elementwise(y, y_ref) >= og.rel_error(y, y_ref)
