@@ -46,7 +46,8 @@ typedef enum {
     SPEC_ERR_ALIGN = 5,        /* pointer or stride misaligned for vector access     */
     SPEC_ERR_WORKSPACE = 6,    /* workspace missing or smaller than required         */
     SPEC_ERR_HIP = 7,          /* a HIP launch failed (see spec_last_hip_error)      */
-    SPEC_ERR_VALUE = 8         /* a scalar argument is out of range (e.g. temperature) */
+    SPEC_ERR_VALUE = 8,        /* a scalar argument is out of range (e.g. temperature) */
+    SPEC_ERR_SCRATCH = 9       /* the call needs more than the library's fixed scratch */
 } spec_status;
 
 typedef enum {
@@ -310,6 +311,32 @@ spec_status spec_verify_accept(const void* target_logits, const void* draft_logi
                                int64_t B, int64_t k, int64_t V, float temperature,
                                int32_t* out_tokens, int32_t* num_accepted,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * spec_verify_accept_noalloc -- spec_verify_accept for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): no workspace argument.  The kernels use
+ * a fixed scratch buffer that the library holds in device memory instead, of
+ * SPEC_ACCEPT_SCRATCH_BYTES (16 MiB) per GPU, held until the process ends.
+ * The scratch is that of the current device (hipGetDevice), which must be
+ * the device of `stream`; its address is looked up on the first call on each
+ * device.  Nothing is allocated or freed, here or in any later call.
+ *
+ * Arguments, requirements and results are those of spec_verify_accept.  A
+ * call whose spec_verify_accept_workspace_bytes(B, k, V) exceeds
+ * SPEC_ACCEPT_SCRATCH_BYTES returns SPEC_ERR_SCRATCH before any HIP call
+ * (at k = 4, V = 128256 that allows B up to about 850).  Every call on one
+ * GPU shares that GPU's scratch and leaves it holding its own intermediate
+ * values (no call depends on what is there on entry), so calls that overlap
+ * on one GPU -- on different streams, or from different threads -- race and
+ * must be serialized by the caller.
+ */
+#define SPEC_ACCEPT_SCRATCH_BYTES ((size_t)16 << 20)
+
+spec_status spec_verify_accept_noalloc(const void* target_logits, const void* draft_logits,
+                                       const int32_t* draft_tokens, const float* uniforms,
+                                       int64_t B, int64_t k, int64_t V, float temperature,
+                                       int32_t* out_tokens, int32_t* num_accepted, void* stream);
 
 /*
  * spec_verify_accept_stats -- spec_verify_accept with the target rows'

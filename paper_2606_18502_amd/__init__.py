@@ -43,6 +43,7 @@ from .ops import (  # noqa: F401
     gemm_silu_mul,
     logit_stats_count,
     verify_accept,
+    verify_accept_noalloc,
     accept_workspace_bytes,
     verify_accept_tree,
     tree_attention_mask,

@@ -8,18 +8,20 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libspecfp8.so")
 
-# enums (include/spec_fp8.h)
+# enums and limits (include/spec_fp8.h)
+ACCEPT_SCRATCH_BYTES = 16 << 20
 SPEC_OK = 0
 STATUS_NAMES = {0: "SPEC_OK", 1: "SPEC_ERR_NULL", 2: "SPEC_ERR_SHAPE", 3: "SPEC_ERR_UNSUPPORTED",
                 4: "SPEC_ERR_ENUM", 5: "SPEC_ERR_ALIGN", 6: "SPEC_ERR_WORKSPACE", 7: "SPEC_ERR_HIP",
-                8: "SPEC_ERR_VALUE"}
+                8: "SPEC_ERR_VALUE", 9: "SPEC_ERR_SCRATCH"}
 SCALE_PER_ROW, SCALE_PER_TENSOR, SCALE_CALIBRATE = 0, 1, 2
 QIN_BF16, QIN_SILU_MUL_BF16 = 0, 1
 OUT_BF16, OUT_F32 = 0, 1
 
 EXPORTS = ("spec_fp8_quantize", "spec_silu_mul_bf16", "spec_fp8_kv_cache_write", "spec_fp8_clip_count", "spec_fp8_gemm_workspace_bytes", "spec_fp8_gemm",
            "spec_fp8_gemm_silu_mul", "spec_logit_stats_count", "spec_fp8_gemm_logit_stats",
-           "spec_verify_accept_workspace_bytes", "spec_verify_accept", "spec_verify_accept_stats",
+           "spec_verify_accept_workspace_bytes", "spec_verify_accept", "spec_verify_accept_noalloc",
+           "spec_verify_accept_stats",
            "spec_verify_accept_tree_workspace_bytes", "spec_verify_accept_tree", "spec_tree_attention_mask",
            "spec_status_string", "spec_last_hip_error", "spec_version")
 
@@ -75,6 +77,8 @@ def load() -> ctypes.CDLL:
     lib.spec_verify_accept_workspace_bytes.restype = sz
     lib.spec_verify_accept.argtypes = [vp, vp, vp, vp, i64, i64, i64, f32, vp, vp, vp, sz, vp]
     lib.spec_verify_accept.restype = i32
+    lib.spec_verify_accept_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i64, f32, vp, vp, vp]
+    lib.spec_verify_accept_noalloc.restype = i32
     lib.spec_status_string.argtypes = [i32]
     lib.spec_status_string.restype = ctypes.c_char_p
     lib.spec_last_hip_error.argtypes = []

@@ -32,8 +32,16 @@
 // position where sampling happens (<= 2 rows per sequence), with every load of
 // a thread issued before it computes.  All reductions use a fixed order, so
 // results are deterministic.
+#include <mutex>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
+
+// Fixed acceptance scratch for callers that cannot allocate
+// (spec_verify_accept_noalloc).  Each GPU holds its own copy at its own
+// address; host code reaches it only through the address accept_scratch()
+// looks up, never through this name (a host-side stand-in).
+static __device__ __align__(256) unsigned char scratch[specfp8::kAcceptScratchBytes];
 
 namespace specfp8 {
 
@@ -1028,7 +1036,28 @@ __global__ __launch_bounds__(256) void clear_tickets_kernel(unsigned int* ctr, i
 
 inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
 }  // namespace
+
+hipError_t accept_scratch(void** ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {
     AcceptPlan p{};

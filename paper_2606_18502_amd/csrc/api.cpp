@@ -152,6 +152,24 @@ spec_status spec_verify_accept(const void* target_logits, const void* draft_logi
                                            as_stream(stream)));
 }
 
+spec_status spec_verify_accept_noalloc(const void* target_logits, const void* draft_logits,
+                                       const int32_t* draft_tokens, const float* uniforms, int64_t B, int64_t k,
+                                       int64_t V, float temperature, int32_t* out_tokens, int32_t* num_accepted,
+                                       void* stream) {
+    const spec_status st = specfp8::check_accept(target_logits, draft_logits, draft_tokens, uniforms, B, k, V,
+                                                 temperature, out_tokens, num_accepted);
+    if (st != SPEC_OK || B == 0) return st;
+    const specfp8::AcceptPlan plan = specfp8::plan_accept(B, k, V);
+    if (plan.bytes > specfp8::kAcceptScratchBytes) return SPEC_ERR_SCRATCH;
+    void* ws = nullptr;
+    const spec_status se = from_hip(specfp8::accept_scratch(&ws));
+    if (se != SPEC_OK) return se;
+    return from_hip(specfp8::launch_accept(plan, reinterpret_cast<const uint16_t*>(target_logits),
+                                           reinterpret_cast<const uint16_t*>(draft_logits), draft_tokens, uniforms,
+                                           B, k, V, temperature, out_tokens, num_accepted, ws,
+                                           as_stream(stream)));
+}
+
 spec_status spec_verify_accept_stats(const void* target_logits, const float* target_stats, int64_t n_stats,
                                      int64_t ld_stats, const void* draft_logits, const int32_t* draft_tokens,
                                      const float* uniforms, int64_t B, int64_t k, int64_t V, float temperature,
@@ -210,6 +228,7 @@ const char* spec_status_string(spec_status s) {
         case SPEC_ERR_WORKSPACE: return "workspace missing or too small";
         case SPEC_ERR_HIP: return "HIP launch failed";
         case SPEC_ERR_VALUE: return "scalar argument out of range";
+        case SPEC_ERR_SCRATCH: return "call exceeds the library's fixed scratch buffer";
     }
     return "unknown status";
 }

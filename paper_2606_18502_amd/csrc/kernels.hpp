@@ -67,6 +67,11 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
                          int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream,
                          const float2* tstats = nullptr, int64_t n_tstats = 0, int64_t ld_tstats = 0);
 
+// Device address of the library's fixed acceptance scratch on the current
+// device (looked up once per device); kAcceptScratchBytes long.
+constexpr size_t kAcceptScratchBytes = (size_t)16 << 20;
+hipError_t accept_scratch(void** ptr);
+
 // Token-tree verification (N nodes per sequence, N+1 target rows); the plan
 // is plan_accept(B, N, V).
 hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int32_t* parent, const int32_t* x,

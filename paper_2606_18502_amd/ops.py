@@ -354,6 +354,42 @@ def verify_accept(target_logits: torch.Tensor, draft_logits: Optional[torch.Tens
     return out_tokens, num_accepted
 
 
+def verify_accept_noalloc(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor],
+                          draft_tokens: torch.Tensor, uniforms: Optional[torch.Tensor], temperature: float,
+                          out_tokens: torch.Tensor, num_accepted: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+    """verify_accept through spec_verify_accept_noalloc: no workspace, the
+    library's fixed device scratch instead, and no allocation here either (the
+    outputs are the caller's).  Same arguments and results as verify_accept."""
+    lib = _lib.load()
+    _dev(target_logits, torch.bfloat16, "target_logits")
+    B, k1, V = target_logits.shape
+    k = k1 - 1
+    if not target_logits.is_contiguous():
+        raise ValueError("target_logits must be contiguous")
+    if draft_logits is not None:
+        _dev(draft_logits, torch.bfloat16, "draft_logits")
+        if tuple(draft_logits.shape) != (B, k, V) or not draft_logits.is_contiguous():
+            raise ValueError("draft_logits must be contiguous [B,k,V]")
+    _dev(draft_tokens, torch.int32, "draft_tokens")
+    if tuple(draft_tokens.shape) != (B, k) or not draft_tokens.is_contiguous():
+        raise ValueError("draft_tokens must be contiguous [B,k]")
+    if uniforms is not None:
+        _dev(uniforms, torch.float32, "uniforms")
+        if tuple(uniforms.shape) != (B, k1) or not uniforms.is_contiguous():
+            raise ValueError("uniforms must be contiguous [B,k+1]")
+    _dev(out_tokens, torch.int32, "out_tokens")
+    _dev(num_accepted, torch.int32, "num_accepted")
+    if tuple(out_tokens.shape) != (B, k1) or not out_tokens.is_contiguous():
+        raise ValueError("out_tokens must be contiguous [B,k+1]")
+    if tuple(num_accepted.shape) != (B,) or not num_accepted.is_contiguous():
+        raise ValueError("num_accepted must be contiguous [B]")
+    check("spec_verify_accept_noalloc", lib.spec_verify_accept_noalloc(
+        target_logits.data_ptr(), None if draft_logits is None else draft_logits.data_ptr(),
+        draft_tokens.data_ptr(), None if uniforms is None else uniforms.data_ptr(), B, k, V,
+        float(temperature), out_tokens.data_ptr(), num_accepted.data_ptr(), _stream()))
+    return out_tokens, num_accepted
+
+
 def accept_tree_workspace_bytes(B: int, N: int, V: int) -> int:
     return int(_lib.load().spec_verify_accept_tree_workspace_bytes(B, N, V))
 

@@ -11,7 +11,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "spec_fp8.h")
 
-OK, NULL, SHAPE, UNSUP, ENUM, ALIGN, WS, HIP, VALUE = range(9)
+OK, NULL, SHAPE, UNSUP, ENUM, ALIGN, WS, HIP, VALUE, SCRATCH = range(10)
 A16 = 0x10000            # fake, 16-byte aligned device address: never dereferenced here
 A1 = 0x10001             # misaligned
 
@@ -41,8 +41,9 @@ def test_exports_every_declared_symbol(lib):
 
 def test_version_and_status_strings(lib):
     assert lib.spec_version() == 510
-    for s in range(9):
+    for s in range(10):
         assert lib.spec_status_string(s)
+    assert lib.spec_status_string(9) != b"unknown status"
     assert lib.spec_status_string(99) == b"unknown status"
     assert lib.spec_last_hip_error() == 0
 
@@ -214,6 +215,28 @@ def test_accept_validation(lib):
     assert acc(lib, wsb=need - 1) == WS
     assert acc(lib, ws=A16 + 8, wsb=need) == ALIGN
     assert acc(lib, B=0, zt=None, zd=None, x=None, u=None, out=None, num=None, ws=None, wsb=0) == OK
+
+
+def accn(lib, zt=A16, zd=A16, x=A16, u=A16, B=2, k=3, V=256, T=0.7, out=A16, num=A16):
+    return lib.spec_verify_accept_noalloc(zt, zd, x, u, B, k, V, ctypes.c_float(T), out, num, None)
+
+
+def test_accept_noalloc_validation(lib):
+    # the argument checks of spec_verify_accept, before any HIP call
+    assert accn(lib, T=float("nan")) == VALUE
+    assert accn(lib, k=0) == SHAPE
+    assert accn(lib, k=17) == UNSUP
+    assert accn(lib, zt=None) == NULL
+    assert accn(lib, u=None) == NULL
+    assert accn(lib, zt=A1) == ALIGN
+    assert accn(lib, B=0, zt=None, zd=None, x=None, u=None, out=None, num=None) == OK
+    # then the fixed scratch's size: the C4 workload fits, a call needing more is refused
+    from paper_2606_18502_amd import _lib
+    limit = _lib.ACCEPT_SCRATCH_BYTES
+    assert lib.spec_verify_accept_workspace_bytes(64, 4, 128256) <= limit
+    assert lib.spec_verify_accept_workspace_bytes(64, 4, 1 << 22) > limit
+    assert accn(lib, B=64, k=4, V=1 << 22) == SCRATCH
+    assert accn(lib, B=64, k=4, V=1 << 22, T=0.0, u=None) == SCRATCH
 
 
 def test_workspace_sizes_grow_with_problem(lib):
