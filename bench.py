@@ -95,7 +95,7 @@ class Step:
         self.y = {n: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for n, (N, K) in self.lin.items()}
         self.h = torch.empty((M, self.lin["gate_up"][0] // 2), dtype=torch.bfloat16, device=dev)
         ws = max(p.gemm_workspace_bytes(M, N, K) for N, K in self.lin.values())
-        self.gws = torch.empty((max(ws, 16),), dtype=torch.uint8, device=dev)
+        self.gws = torch.zeros((max(ws, 16),), dtype=torch.uint8, device=dev)
         B, k, V = cfg4["B"], cfg4["k"], cfg4["V"]
         self.T = cfg4["temperature"]
         self.aws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device=dev)
@@ -320,7 +320,7 @@ def draft_and_kv_parts(torch, p, wl, step, reps=22, copies=2):
         wcopies.append(ws)
     q = {n: torch.empty((M, K), dtype=torch.uint8, device=dev) for n, (N, K) in lin.items()}
     y = {n: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for n, (N, K) in lin.items()}
-    gws = torch.empty((max(16, max(p.gemm_workspace_bytes(M, N, K) for N, K in lin.values())),),
+    gws = torch.zeros((max(16, max(p.gemm_workspace_bytes(M, N, K) for N, K in lin.values())),),
                       dtype=torch.uint8, device=dev)
     scale = {n: torch.zeros(1, dtype=torch.float32, device=dev) for n in lin}
     for n in acts:
@@ -504,7 +504,7 @@ def other_configs(torch, p, wl, reps=12):
         ncp = max(2, int(np.ceil(300e6 / (N * K))))
         wq = [p.quantize(torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)) for _ in range(ncp)]
         out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-        ws = torch.empty((max(16, p.gemm_workspace_bytes(M, N, K)),), dtype=torch.uint8, device="cuda")
+        ws = torch.zeros((max(16, p.gemm_workspace_bytes(M, N, K)),), dtype=torch.uint8, device="cuda")
         us = timed(lambda r: p.gemm(a, sa, *wq[r % ncp], out=out, workspace=ws), ncp)
         nbytes = M * K + N * K + 4 * (M + N) + 2 * M * N
         c2res[name + "_us"] = round(us, 1)
@@ -524,7 +524,7 @@ def other_configs(torch, p, wl, reps=12):
         a, sa = p.quantize(torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16))
         wq = [p.quantize(torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)) for _ in range(3)]
         out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-        ws = torch.empty((max(16, p.gemm_workspace_bytes(M, N, K)),), dtype=torch.uint8, device="cuda")
+        ws = torch.zeros((max(16, p.gemm_workspace_bytes(M, N, K)),), dtype=torch.uint8, device="cuda")
         fl = 2.0 * M * N * K
         us = timed(lambda r: p.gemm(a, sa, *wq[r % 3], out=out, workspace=ws), 3)
         c5res[name + "_us"] = round(us, 1)
@@ -817,7 +817,7 @@ def profile_traffic(torch, p, wl):
     ws = [torch.randint(0, 120, (N, K), dtype=torch.uint8, device="cuda") for _ in range(3)]
     sw = torch.rand(N, device="cuda") * 0.01 + 1e-3
     out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    wsb = torch.empty((max(p.gemm_workspace_bytes(M, N, K), 16),), dtype=torch.uint8, device="cuda")
+    wsb = torch.zeros((max(p.gemm_workspace_bytes(M, N, K), 16),), dtype=torch.uint8, device="cuda")
     for i in range(3):
         p.gemm(a, sa, ws[i], sw, out=out, workspace=wsb)
     torch.cuda.synchronize()
@@ -835,7 +835,7 @@ def profile_gemm_c5(torch, p, wl):
     ws = [torch.randint(0, 120, (N, K), dtype=torch.uint8, device="cuda") for _ in range(3)]
     sw = torch.rand(N, device="cuda") * 0.01 + 1e-3
     out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    wsb = torch.empty((max(p.gemm_workspace_bytes(M, N, K), 16),), dtype=torch.uint8, device="cuda")
+    wsb = torch.zeros((max(p.gemm_workspace_bytes(M, N, K), 16),), dtype=torch.uint8, device="cuda")
     for i in range(3):
         p.gemm(a, sa, ws[i], sw, out=out, workspace=wsb)
     torch.cuda.synchronize()

@@ -195,7 +195,13 @@ spec_status spec_fp8_kv_cache_write(const void* k, int64_t ld_k, const void* v, 
  * a_scale fp32 [M] (PER_ROW) or [1] (PER_TENSOR); w_scale fp32 [N] or [1].
  * Y       bf16 or fp32 [M, ldy], N <= ldy.
  * workspace  device scratch of at least spec_fp8_gemm_workspace_bytes(M,N,K)
- *         bytes (may be NULL when that is 0); contents on entry are ignored.
+ *         bytes (may be NULL when that is 0), 16-byte aligned.  Where the
+ *         K dimension is split over workgroups, its first 16 KiB hold one
+ *         ticket per output tile: they must be zero before the first call that
+ *         uses the workspace (fill it with zeros once, e.g. when allocating),
+ *         and every call leaves them zero again, so one workspace serves every
+ *         later call of any shape.  The rest of it is overwritten.  Calls that
+ *         share a workspace must not overlap (one stream, or serialized).
  * Requirements: M >= 0 (0 is a no-op), N > 0, K > 0, K % 128 == 0 (else
  * SPEC_ERR_UNSUPPORTED); lda % 16 == 0, ldw % 16 == 0, A and W 16-byte
  * aligned; ldy % 8 == 0 and Y 16-byte aligned.  M and N need not be tile

@@ -25,7 +25,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libspecfp8.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["quantize.hip", "kvcache.hip", "gemm.hip", "accept.hip", "tree_mask.hip", "api.cpp"]
+HIP_SOURCES = ["quantize.hip", "kvcache.hip", "gemm.hip", "accept.hip", "tree_mask.hip", "api.cpp", "plan.cpp"]
 HOST_SOURCES = ["validate.cpp"]
 
 

@@ -36,6 +36,7 @@
 
 #include "device_common.hpp"
 #include "kernels.hpp"
+#include "plan.hpp"
 
 // Fixed acceptance scratch for callers that cannot allocate
 // (spec_verify_accept_noalloc).  Each GPU holds its own copy at its own
@@ -47,12 +48,13 @@ namespace specfp8 {
 
 namespace {
 
-constexpr int kAThreads = 256;
+constexpr int kAThreads = kAcceptThreads;
 constexpr int kWavesPerBlock = kAThreads / kWave;
-constexpr int kVecs = 8;                               // 16-byte vectors per lane per item
-constexpr int64_t kSlice = (int64_t)kWave * kVecs * 8;         // 4096 logits per wave item
-constexpr int kPerThread = kVecs * 8;                  // 64 logits per thread (sample kernel)
-constexpr int64_t kChunk = (int64_t)kAThreads * kPerThread;   // 16384 logits per sample block
+constexpr int kVecs = kAcceptVecs;                     // 16-byte vectors per lane per item
+constexpr int64_t kSlice = kAcceptSlice;               // 4096 logits per wave item
+constexpr int kPerThread = kAcceptPerThread;           // 64 logits per thread (sample kernel)
+constexpr int64_t kChunk = kAcceptChunk;               // 16384 logits per sample block
+static_assert(kSlice == (int64_t)kWave * kVecs * 8 && kChunk == (int64_t)kAThreads * kPerThread, "accept geometry");
 constexpr int kMaxChunks = kAThreads;                 // V <= 2^22: one chunk per thread
 constexpr int kStreamWavesPerCU = 12;
 constexpr int kCUs = 256;
@@ -1034,8 +1036,6 @@ __global__ __launch_bounds__(256) void clear_tickets_kernel(unsigned int* ctr, i
     if (i < n) ctr[i] = 0u;
 }
 
-inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
-
 constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mutex;
 void* g_scratch_ptr[kMaxDevices] = {};
@@ -1057,22 +1057,6 @@ hipError_t accept_scratch(void** ptr) {
     }
     *ptr = g_scratch_ptr[dev];
     return hipSuccess;
-}
-
-AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {
-    AcceptPlan p{};
-    p.chunk = kChunk;
-    p.nchunk = (V + kChunk - 1) / kChunk;
-    p.schunk = kSlice;
-    p.nschunk = (V + kSlice - 1) / kSlice;
-    const int64_t R = 2 * k + 1;
-    p.stats_off = 0;
-    p.mass_off = align256((size_t)B * R * p.nschunk * sizeof(float2));
-    p.fine_off = p.mass_off + align256((size_t)B * p.nchunk * sizeof(double));
-    p.ctr_off = p.fine_off + align256((size_t)B * p.nchunk * kAThreads * sizeof(double));
-    p.bytes = p.ctr_off + align256((size_t)B * sizeof(unsigned int));
-    if (B == 0) p.bytes = 0;
-    return p;
 }
 
 hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t* zd, const int32_t* x,

@@ -22,8 +22,10 @@
 //    while the current one is multiplied.
 //
 // K is split across workgroups (split-K) when there are fewer output tiles
-// than compute units; partial fp32 tiles then go to a workspace and a second
-// kernel adds them in split order (deterministic) and applies the epilogue.
+// than compute units.  The fp32 partial tiles are then added in split order
+// (deterministic), either by the last workgroup of each tile to finish (a
+// ticket per tile; it then applies the epilogue) or, for many splits of small
+// tiles, by a second kernel.
 // Workgroup ids are remapped so that the tiles and K-splits that share
 // operands run on the same XCD (blocks are dealt round-robin to the 8 XCDs),
 // which keeps re-read operand bytes in that XCD's L2.
@@ -39,12 +41,7 @@
 
 #include "device_common.hpp"
 #include "kernels.hpp"
-
-#ifdef SPECFP8_TUNING
-#include <stdio.h>
-#include <stdlib.h>
-#endif
-
+#include "plan.hpp"
 
 namespace specfp8 {
 
@@ -54,7 +51,7 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 namespace {
 
-constexpr int kBK = 128;     // bytes (= E4M3 elements) of K per step
+constexpr int kBK = kGemmBK;   // bytes (= E4M3 elements) of K per step
 constexpr int kXcds = 8;
 
 struct GemmArgs {
@@ -63,7 +60,10 @@ struct GemmArgs {
     const float* sa;
     const float* sw;
     void* y;
-    float* partial;   // [splits][M][ldp] when splits > 1
+    float* partial;   // kReduceKernel: [splits][M][ldp]
+    uint64_t* part;   // kReduceLast: per tile and split, the threads' accumulators (two 8-byte halves each)
+    unsigned int* tickets;   // kReduceLast: one per tile, zero between calls
+    int reduce;       // GemmReduce of the plan
     float2* stats;    // [M][ld_stats] column-group statistics of the bf16 output (stats_mode != 0)
     int64_t lda, ldw, ldy, ldp, ld_stats;
     int M, N, K;
@@ -150,14 +150,8 @@ __device__ __forceinline__ void issue_stage(const GemmArgs& g, char* stage, int 
 // over 8 of the step's MFMA count): the LDS reads of the next step are spread
 // over the first kReadSpan8/8 of the MFMAs, so they have completed by the end
 // of the step, and the stage refill loads over the first kLoadSpan8/8.
-#ifndef SPECFP8_READ_SPAN8
-#define SPECFP8_READ_SPAN8 5
-#endif
-#ifndef SPECFP8_LOAD_SPAN8
-#define SPECFP8_LOAD_SPAN8 4
-#endif
-constexpr int kReadSpan8 = SPECFP8_READ_SPAN8;
-constexpr int kLoadSpan8 = SPECFP8_LOAD_SPAN8;
+constexpr int kReadSpan8 = 5;
+constexpr int kLoadSpan8 = 4;
 
 // vmcnt(N) with lgkmcnt/expcnt left alone (vmcnt field: bits [3:0] and [15:14]).
 template <int N>
@@ -335,7 +329,7 @@ __device__ __forceinline__ void store_blocks(const GemmArgs& g, const v4f (&acc)
                                              float (&ss)[WTM]) {
     const int kg = lane >> 4;
     const int r16 = lane & 15;
-    if (STATS == 0 && g.splits > 1) {
+    if (STATS == 0 && g.splits > 1 && g.reduce == kReduceKernel) {
 #pragma unroll
         for (int j = 0; j < WTM; ++j) {
             const int m = m0 + (wm * WTM + j) * 16 + r16;
@@ -488,7 +482,89 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[W
     }
 }
 
-template <int WTM, int WTN, int WM, int WN, int STAGES, int STATS>
+__device__ __forceinline__ uint64_t pack2(float lo, float hi) {
+    return ((uint64_t)__float_as_uint(hi) << 32) | (uint64_t)__float_as_uint(lo);
+}
+
+// Split-K reduced in the kernel (kReduceLast).  Every workgroup of a split
+// tile stores its fp32 partial tile with device-coherent stores (relaxed
+// agent-scope atomics: written through the non-coherent caches, so a
+// workgroup on any XCD reads them), waits until all of them are
+// acknowledged, then takes the tile's ticket.  The workgroup that takes the
+// last ticket -- every other partial is then already acknowledged -- reloads
+// them with device-coherent loads issued after the ticket returned, and adds
+// all of them in split order, its own from registers, so the sums do not
+// depend on which workgroup arrives last.  It returns the ticket to zero for
+// the next call.  Each thread stores and reloads exactly the accumulators it
+// holds (one float4 per 16x16 block, as two 8-byte halves in separate
+// 512-byte rows, so every store and load instruction of a wave is contiguous).
+// Returns false in the workgroups that are not last (they are done).
+template <int WTM, int WTN, int NT>
+__device__ __forceinline__ bool reduce_last(const GemmArgs& g, v4f (&acc)[WTN][WTM], int tile, int split, int tid,
+                                            int* s_flag) {
+    constexpr int kBlocks = WTM * WTN;
+    uint64_t* const base = g.part + (size_t)tile * g.splits * kBlocks * 2 * NT;
+    {
+        uint64_t* const mine = base + (size_t)split * kBlocks * 2 * NT + tid;
+#pragma unroll
+        for (int i = 0; i < WTN; ++i)
+#pragma unroll
+            for (int j = 0; j < WTM; ++j) {
+                uint64_t* p = mine + (size_t)(i * WTM + j) * 2 * NT;
+                __hip_atomic_store(p, pack2(acc[i][j][0], acc[i][j][1]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(p + NT, pack2(acc[i][j][2], acc[i][j][3]), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            }
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0) {
+        const unsigned int t = __hip_atomic_fetch_add(g.tickets + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int last = t == (unsigned int)(g.splits - 1);
+        if (last) __hip_atomic_store(g.tickets + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *s_flag = last;
+    }
+    __syncthreads();
+    if (!*s_flag) return false;
+    v4f tot[WTN][WTM];
+    for (int z = 0; z < g.splits; ++z) {
+        v4f part[WTN][WTM];
+        if (z == split) {
+#pragma unroll
+            for (int i = 0; i < WTN; ++i)
+#pragma unroll
+                for (int j = 0; j < WTM; ++j) part[i][j] = acc[i][j];
+        } else {
+            const uint64_t* src = base + (size_t)z * kBlocks * 2 * NT + tid;
+            uint64_t lo[WTN][WTM], hi[WTN][WTM];
+#pragma unroll
+            for (int i = 0; i < WTN; ++i)
+#pragma unroll
+                for (int j = 0; j < WTM; ++j) {
+                    const uint64_t* p = src + (size_t)(i * WTM + j) * 2 * NT;
+                    lo[i][j] = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    hi[i][j] = __hip_atomic_load(p + NT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+#pragma unroll
+            for (int i = 0; i < WTN; ++i)
+#pragma unroll
+                for (int j = 0; j < WTM; ++j)
+                    part[i][j] = v4f{__uint_as_float((uint32_t)lo[i][j]), __uint_as_float((uint32_t)(lo[i][j] >> 32)),
+                                     __uint_as_float((uint32_t)hi[i][j]), __uint_as_float((uint32_t)(hi[i][j] >> 32))};
+        }
+#pragma unroll
+        for (int i = 0; i < WTN; ++i)
+#pragma unroll
+            for (int j = 0; j < WTM; ++j) tot[i][j] = z == 0 ? part[i][j] : tot[i][j] + part[i][j];
+    }
+#pragma unroll
+    for (int i = 0; i < WTN; ++i)
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) acc[i][j] = tot[i][j];
+    return true;
+}
+
+template <int WTM, int WTN, int WM, int WN, int STAGES, int STATS, bool REDUCE_LAST>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     using C = GemmCfg<WTM, WTN, WM, WN, STAGES>;
     static_assert(STAGES >= 2 && STAGES <= 4, "2..4 stages");
@@ -586,6 +662,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
 #undef SPEC_STEP
     wait_vmcnt<0>();   // no direct-to-LDS write may outlive the workgroup
 
+    if constexpr (STATS == 0 && REDUCE_LAST) {
+        if (g.splits > 1 && g.reduce == kReduceLast) {
+            __shared__ int s_last;
+            if (!reduce_last<WTM, WTN, C::kThreads>(g, acc, tile, split, tid, &s_last)) return;
+        }
+    }
     store_tile<WTM, WTN, WN, STATS>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, nt, C::BM, C::BN);
 }
 
@@ -629,144 +711,43 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g) {
     }
 }
 
-// ---- tile configurations -------------------------------------------------
-// kind  BM x BN   waves (wave tile)     stages  LDS      used for
-//  0    64 x 64   2x2 (32x32)           4       64 KiB   M <= 64
-//  1    80 x 128  1x2 (80x64)           4       104 KiB  M <= 80
-//  2   160 x 224  2x2 (80x112)          3       144 KiB  M <= 320, N % 224 == 0
-//  3   256 x 128  2x2 (128x64)          3       144 KiB  large M
-//  4   160 x 192  2x2 (80x96)           3       132 KiB  M <= 320, N % 192 == 0
-//  5   160 x 128  2x2 (80x64)           4       144 KiB  M <= 320
-//  6   320 x 64   4x1 (80x64)           3       144 KiB
-//  7   160 x 64   2x2 (80x32)           4       112 KiB
-//  8    64 x 128  2x2 (32x64)           4        96 KiB   M <= 320, short N (QKV, O)
-using Cfg0 = GemmCfg<2, 2, 2, 2, 4>;
-using Cfg1 = GemmCfg<5, 4, 1, 2, 4>;
-using Cfg2 = GemmCfg<5, 7, 2, 2, 3>;
-using Cfg3 = GemmCfg<8, 4, 2, 2, 3>;
-using Cfg4 = GemmCfg<5, 6, 2, 2, 3>;
-using Cfg5 = GemmCfg<5, 4, 2, 2, 4>;
-using Cfg6 = GemmCfg<5, 4, 4, 1, 3>;
-using Cfg7 = GemmCfg<5, 2, 2, 2, 4>;
-using Cfg8 = GemmCfg<2, 4, 2, 2, 4>;
-constexpr int kKinds = 9;
-
-constexpr int kCfgBM[kKinds] = {Cfg0::BM, Cfg1::BM, Cfg2::BM, Cfg3::BM, Cfg4::BM, Cfg5::BM, Cfg6::BM, Cfg7::BM, Cfg8::BM};
-constexpr int kCfgBN[kKinds] = {Cfg0::BN, Cfg1::BN, Cfg2::BN, Cfg3::BN, Cfg4::BN, Cfg5::BN, Cfg6::BN, Cfg7::BN, Cfg8::BN};
-constexpr int kCfgWN[kKinds] = {2, 2, 2, 2, 2, 2, 1, 2, 2};   // waves across N (statistics groups per tile)
+// ---- tile configurations (plan.hpp, kTiles) ----------------------------------
 
 // The statistics epilogues are separate instantiations, so the plain GEMMs'
 // register allocation does not carry them (and the 160x224 tile, whose
 // statistics variant would spill, has none: the plan never asks for it).
-template <class C, int WTM, int WTN, int WM, int WN, int STAGES, bool WITH_STATS = true>
+template <int KIND, bool WITH_STATS = true, bool REDUCE_LAST = true>
 hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
+    constexpr int WTM = kTiles[KIND].wtm, WTN = kTiles[KIND].wtn, WM = kTiles[KIND].wm, WN = kTiles[KIND].wn;
+    constexpr int STAGES = kTiles[KIND].stages;
+    using C = GemmCfg<WTM, WTN, WM, WN, STAGES>;
+    static_assert(C::BM == tile_bm(KIND) && C::BN == tile_bn(KIND), "tile table");
     const int total = g.m_tiles * g.n_tiles * g.splits;
     if (g.silu_inter > 0) {
-        hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 3>), dim3(total), dim3(C::kThreads), 0,
+        hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 3, false>), dim3(total), dim3(C::kThreads), 0,
                            stream, g);
         return hipGetLastError();
     }
     if constexpr (WITH_STATS) {
         if (g.stats_mode == 1) {
-            hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 1>), dim3(total), dim3(C::kThreads), 0,
+            hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 1, false>), dim3(total), dim3(C::kThreads), 0,
                                stream, g);
             return hipGetLastError();
         }
         if (g.stats_mode == 2) {
-            hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 2>), dim3(total), dim3(C::kThreads), 0,
+            hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 2, false>), dim3(total), dim3(C::kThreads), 0,
                                stream, g);
             return hipGetLastError();
         }
     }
     if (g.stats_mode != 0) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 0>), dim3(total), dim3(C::kThreads), 0, stream, g);
+    if (!REDUCE_LAST && g.splits > 1 && g.reduce == kReduceLast) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 0, REDUCE_LAST>), dim3(total), dim3(C::kThreads), 0,
+                       stream, g);
     return hipGetLastError();
 }
 
 }  // namespace
-
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
-    GemmPlan p{};
-    const bool no_split = epilogue != kEpiPlain;
-    // Tile shapes by measurement on MI355X (M = B*(k+1) verify rows):
-    //   M <= 80: 64x64 with K split (below), but for very wide N (gate|up)
-    //            64x128 (M <= 64) or 80x128 unsplit;
-    //   M <= 320: 160x224 when N fills >= 64 such columns exactly (gate|up),
-    //             else for very wide N (an LM head) 160x192 (or 160x224
-    //             with a ragged last tile),
-    //             160x128 with a K split for long-K layers (down), else
-    //             64x128 (QKV, O: a CU's time is set by the operand rows it
-    //             streams per K-step, 192 here against 224 for 160x64);
-    //   larger M: 160x224.
-    if (M <= 80) p.kind = N >= 192 * 64 ? (M <= 64 ? 8 : 1) : 0;
-    else if (M <= 320) {
-        if (N % 224 == 0 && N >= 224 * 64) p.kind = 2;
-        else if (N >= 192 * 64) p.kind = (N % 192 == 0) ? 4 : 2;
-        else p.kind = K >= 2 * N ? 5 : 8;
-    }
-    else p.kind = 2;
-    // with the statistics epilogue the 160x224 tile would spill registers;
-    // 160x192 (ragged last tile where N % 192 != 0) takes its place
-    if (epilogue == kEpiStats && p.kind == 2) p.kind = 4;
-    const int ksteps = (int)(K / kBK);
-    int splits = 0;
-#ifdef SPECFP8_TUNING
-    // tuning builds only: SPECFP8_GEMM_PLAN="kind:splits" overrides the choice
-    if (const char* env = getenv("SPECFP8_GEMM_PLAN")) {
-        int k = -1, sp = 0;
-        if (sscanf(env, "%d:%d", &k, &sp) >= 1 && k >= 0 && k < kKinds) { p.kind = k; splits = sp; }
-    }
-#endif
-    const int bm = kCfgBM[p.kind], bn = kCfgBN[p.kind];
-    p.m_tiles = (int)((M + bm - 1) / bm);
-    p.n_tiles = (int)((N + bn - 1) / bn);
-    const int64_t tiles = (int64_t)p.m_tiles * p.n_tiles;
-    if (no_split) splits = 1;
-    if (splits <= 0 && M <= 80 && p.kind == 0) {
-        // Draft and small verify batches (64x64 tiles): the GEMM is a weight
-        // stream with a fixed cost per workgroup, so K is split until about
-        // 256 workgroups run or every split holds at most 32 K-steps, keeping
-        // at least 8 K-steps per split (the partials are small at this M).
-        splits = (int)(256 / tiles);
-        if (splits < (ksteps + 31) / 32) splits = (ksteps + 31) / 32;
-        const int max_split = ksteps / 8 > 0 ? ksteps / 8 : 1;
-        if (splits > max_split) splits = max_split;
-        if (splits > 16) splits = 16;
-    }
-    if (splits <= 0) {
-        // Split K only when at most half of the 256 compute units would get
-        // a tile, and keep the split grid under ~200 workgroups: every split
-        // adds an M x N fp32 partial that is written and read back.
-        splits = 1;
-        if (2 * tiles <= 256) splits = 200 / tiles;
-        const int max_split = ksteps / 4 > 0 ? ksteps / 4 : 1;   // >= 4 K-steps per split
-        if (splits > max_split) splits = max_split;
-        if (splits > 16) splits = 16;
-    }
-    if (splits > ksteps) splits = ksteps;
-    if (splits < 1) splits = 1;
-    // every split must own at least one K-step after ceil division
-    while (splits > 1 && (int64_t)((ksteps + splits - 1) / splits) * (splits - 1) >= ksteps) --splits;
-    p.splits = splits;
-    // Many M-tiles (long prompts): tiles in groups of 4 M-tiles with K walked
-    // in step, so the 32 tiles an XCD runs at once re-read 4 activation and
-    // 8 weight tiles from its L2 (5-8% at M = 4096).  Few M-tiles keep the
-    // staggered K start, which spreads the requests for shared rows.
-    p.group_m = 1;
-    p.krot_on = 1;
-    if (p.m_tiles >= 8 && splits == 1) {
-        p.group_m = 4;
-        p.krot_on = 0;
-    }
-#ifdef SPECFP8_TUNING
-    if (const char* env = getenv("SPECFP8_GROUP_M")) p.group_m = atoi(env) > 0 ? atoi(env) : 1;
-    if (const char* env = getenv("SPECFP8_KROT")) p.krot_on = atoi(env);
-#endif
-    p.stat_groups = (int64_t)p.n_tiles * kCfgWN[p.kind];
-    p.ldp = (N + 3) / 4 * 4;
-    p.workspace_bytes = splits > 1 ? (size_t)splits * (size_t)M * (size_t)p.ldp * sizeof(float) : 0;
-    return p;
-}
 
 hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const float* sa, int a_per_tensor,
                        const uint8_t* w, int64_t ldw, const float* sw, int w_per_tensor, int64_t M,
@@ -777,7 +758,11 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
     g.stats = stats; g.ld_stats = ld_stats; g.stats_mode = stats_mode; g.c2 = c2;
     g.silu_inter = (int)silu_inter;
     g.a = a; g.w = w; g.sa = sa; g.sw = sw; g.y = y;
-    g.partial = reinterpret_cast<float*>(workspace);
+    char* ws = reinterpret_cast<char*>(workspace);
+    g.tickets = reinterpret_cast<unsigned int*>(ws);
+    g.partial = reinterpret_cast<float*>(ws ? ws + p.part_off : nullptr);
+    g.part = reinterpret_cast<uint64_t*>(ws ? ws + p.part_off : nullptr);
+    g.reduce = p.reduce;
     g.lda = lda; g.ldw = ldw; g.ldy = ldy; g.ldp = p.ldp;
     g.M = (int)M; g.N = (int)N; g.K = (int)K;
     g.a_per_tensor = a_per_tensor; g.w_per_tensor = w_per_tensor; g.out_f32 = out_f32;
@@ -786,17 +771,19 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
     g.krot_on = p.krot_on;
     hipError_t e;
     switch (p.kind) {
-        case 0: e = launch_cfg<Cfg0, 2, 2, 2, 2, 4>(g, stream); break;
-        case 1: e = launch_cfg<Cfg1, 5, 4, 1, 2, 4>(g, stream); break;
-        case 2: e = launch_cfg<Cfg2, 5, 7, 2, 2, 3, false>(g, stream); break;
-        case 3: e = launch_cfg<Cfg3, 8, 4, 2, 2, 3>(g, stream); break;
-        case 4: e = launch_cfg<Cfg4, 5, 6, 2, 2, 3>(g, stream); break;
-        case 5: e = launch_cfg<Cfg5, 5, 4, 2, 2, 4>(g, stream); break;
-        case 6: e = launch_cfg<Cfg6, 5, 4, 4, 1, 3>(g, stream); break;
-        case 7: e = launch_cfg<Cfg7, 5, 2, 2, 2, 4>(g, stream); break;
-        default: e = launch_cfg<Cfg8, 2, 4, 2, 2, 4>(g, stream); break;
+        case 0: e = launch_cfg<0>(g, stream); break;
+        case 1: e = launch_cfg<1>(g, stream); break;
+        case 2: e = launch_cfg<2, false, false>(g, stream); break;
+        case 3: e = launch_cfg<3>(g, stream); break;
+        case 4: e = launch_cfg<4>(g, stream); break;
+        case 5: e = launch_cfg<5>(g, stream); break;
+        case 6: e = launch_cfg<6>(g, stream); break;
+        case 7: e = launch_cfg<7>(g, stream); break;
+        case 8: e = launch_cfg<8>(g, stream); break;
+        default: return hipErrorInvalidValue;
     }
-    if (e != hipSuccess || p.splits == 1) return e;
+    static_assert(kTileKinds == 9, "every tile kind has a case");
+    if (e != hipSuccess || p.splits == 1 || p.reduce != kReduceKernel) return e;
     const int64_t work = M * ((N + 3) / 4);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, stream, g);
     return hipGetLastError();

@@ -1,0 +1,118 @@
+// Host-side planners: tile shape, K split and workspace layout of the FP8
+// GEMM, and the workspace layout of the acceptance.  Plain C++ (no HIP), so
+// the argument checks and plans can also be built and exercised on a host
+// without a GPU.
+#include "kernels.hpp"
+#include "plan.hpp"
+
+namespace specfp8 {
+
+namespace {
+
+inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+}  // namespace
+
+GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int reduce, int epilogue) {
+    GemmPlan p{};
+    if (kind < 0 || kind >= kTileKinds) kind = 2;
+    // the statistics epilogues never split K; the 160x224 tile has no
+    // statistics variant (it would spill), 160x192 takes its place
+    if (epilogue == kEpiStats && kind == 2) kind = 4;
+    if (epilogue != kEpiPlain) splits = 1;
+    p.kind = kind;
+    const int bm = tile_bm(kind), bn = tile_bn(kind);
+    p.m_tiles = (int)((M + bm - 1) / bm);
+    p.n_tiles = (int)((N + bn - 1) / bn);
+    const int ksteps = (int)(K / kGemmBK);
+    if (splits > ksteps) splits = ksteps;
+    if (splits < 1) splits = 1;
+    // every split must own at least one K-step after ceil division
+    while (splits > 1 && (int64_t)((ksteps + splits - 1) / splits) * (splits - 1) >= ksteps) --splits;
+    p.splits = splits;
+    const int64_t tiles = (int64_t)p.m_tiles * p.n_tiles;
+    if (splits == 1) reduce = kReduceNone;
+    else if (reduce != kReduceKernel && reduce != kReduceLast) reduce = kReduceLast;
+    // the 160x224 kernel has no in-kernel reduction (its registers are full);
+    // more tiles than tickets fall back to the reduction kernel as well
+    if (reduce == kReduceLast && (kind == 2 || tiles > (int64_t)(kGemmTicketBytes / sizeof(unsigned int))))
+        reduce = kReduceKernel;
+    p.reduce = reduce;
+    // Many M-tiles (long prompts): tiles in groups of 4 M-tiles with K walked
+    // in step, so the 32 tiles an XCD runs at once re-read 4 activation and
+    // 8 weight tiles from its L2 (5-8% at M = 4096).  Few M-tiles keep the
+    // staggered K start, which spreads the requests for shared rows.
+    p.group_m = 1;
+    p.krot_on = 1;
+    if (p.m_tiles >= 8 && splits == 1) {
+        p.group_m = 4;
+        p.krot_on = 0;
+    }
+    p.stat_groups = (int64_t)p.n_tiles * kTiles[kind].wn;
+    p.ldp = (N + 3) / 4 * 4;
+    p.part_off = kGemmTicketBytes;
+    if (reduce == kReduceKernel)
+        p.workspace_bytes = p.part_off + align256((size_t)splits * (size_t)M * (size_t)p.ldp * sizeof(float));
+    else if (reduce == kReduceLast)
+        p.workspace_bytes = p.part_off + align256((size_t)tiles * splits * (size_t)bm * bn * sizeof(float));
+    else
+        p.workspace_bytes = 0;
+    return p;
+}
+
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
+    const int ksteps = (int)(K / kGemmBK);
+    int splits = 1;
+    // Tile shapes by measurement on MI355X (M = B*(k+1) verify rows).
+    if (M <= 80) {
+        // Draft and small verify batches: a weight stream with a fixed cost
+        // per workgroup.  Very wide N (gate|up) fills the chip unsplit;
+        // otherwise 64x64 tiles with K split until about 256 workgroups run
+        // or every split holds at most 32 K-steps, keeping >= 8 K-steps per
+        // split.
+        if (N >= 192 * 64) return plan_gemm_as(M, N, K, M <= 64 ? 8 : 1, 1, kReduceNone, epilogue);
+        const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);
+        splits = (int)(256 / tiles);
+        if (splits < (ksteps + 31) / 32) splits = (ksteps + 31) / 32;
+        const int max_split = ksteps / 8 > 0 ? ksteps / 8 : 1;
+        if (splits > max_split) splits = max_split;
+        if (splits > 16) splits = 16;
+        return plan_gemm_as(M, N, K, 0, splits, kReduceKernel, epilogue);
+    }
+    if (M <= 320) {
+        // wide N: one 160x224 tile per CU (gate|up), or 160x192 for an LM
+        // head (160x224 with a ragged last tile where N % 192 != 0)
+        if (N % 224 == 0 && N >= 224 * 64) return plan_gemm_as(M, N, K, 2, 1, kReduceNone, epilogue);
+        if (N >= 192 * 64) return plan_gemm_as(M, N, K, (N % 192 == 0) ? 4 : 2, 1, kReduceNone, epilogue);
+        // Short N (QKV, O, down).  A CU streams its operand rows at a rate
+        // that no tile shape or wave count tried raised (~35 GB/s per CU at
+        // every shape of the verify step), so a CU's time follows the operand
+        // bytes it streams; a K split pays when it brings idle CUs in, and its
+        // partial tiles are added by the last workgroup of each tile.  Sweeps
+        // (cold weights) chose: long K (down, 14336 -> 4096) 80x128 tiles with
+        // K split in 2; N <= 4096 (O) 160x64 split in 2; else (QKV) 64x128
+        // unsplit.
+        if (K >= 2 * N) return plan_gemm_as(M, N, K, 1, 2, kReduceLast, epilogue);
+        if (N <= 4096) return plan_gemm_as(M, N, K, 7, 2, kReduceLast, epilogue);
+        return plan_gemm_as(M, N, K, 8, 1, kReduceNone, epilogue);
+    }
+    return plan_gemm_as(M, N, K, 2, 1, kReduceNone, epilogue);
+}
+
+AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {
+    AcceptPlan p{};
+    p.chunk = kAcceptChunk;
+    p.nchunk = (V + kAcceptChunk - 1) / kAcceptChunk;
+    p.schunk = kAcceptSlice;
+    p.nschunk = (V + kAcceptSlice - 1) / kAcceptSlice;
+    const int64_t R = 2 * k + 1;
+    p.stats_off = 0;
+    p.mass_off = align256((size_t)B * R * p.nschunk * 8);     // float2 per (row, slice)
+    p.fine_off = p.mass_off + align256((size_t)B * p.nchunk * sizeof(double));
+    p.ctr_off = p.fine_off + align256((size_t)B * p.nchunk * kAcceptThreads * sizeof(double));
+    p.bytes = p.ctr_off + align256((size_t)B * sizeof(unsigned int));
+    if (B == 0) p.bytes = 0;
+    return p;
+}
+
+}  // namespace specfp8

@@ -1,0 +1,55 @@
+// Launch geometry shared by the host-side planners (plan.cpp) and the
+// kernels (gemm.hip, accept.hip).  Host-only code: no HIP here.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace specfp8 {
+
+// ---- FP8 GEMM tiles ---------------------------------------------------------
+// A tile is a WM x WN grid of waves, each wave holding WTM x WTN blocks of
+// 16x16 outputs; STAGES LDS buffers rotate through the K-loop.
+struct TileShape {
+    int wtm, wtn, wm, wn, stages;
+};
+
+// kind  BM x BN   waves (wave tile)     stages  LDS      used for
+//  0    64 x 64   2x2 (32x32)           4       64 KiB   M <= 80 (K split)
+//  1    80 x 128  1x2 (80x64)           4       104 KiB  M <= 80 wide N; M <= 320 long K (split)
+//  2   160 x 224  2x2 (80x112)          3       144 KiB  M <= 320 wide N, large M
+//  3   256 x 128  2x2 (128x64)          3       144 KiB
+//  4   160 x 192  2x2 (80x96)           3       132 KiB  wide N with statistics
+//  5   160 x 128  2x2 (80x64)           4       144 KiB
+//  6   320 x 64   4x1 (80x64)           3       144 KiB
+//  7   160 x 64   2x2 (80x32)           4       112 KiB  M <= 320, N <= 4096 (split)
+//  8    64 x 128  2x2 (32x64)           4        96 KiB  M <= 64 wide N; M <= 320 short N
+constexpr TileShape kTiles[] = {
+    {2, 2, 2, 2, 4}, {5, 4, 1, 2, 4}, {5, 7, 2, 2, 3}, {8, 4, 2, 2, 3}, {5, 6, 2, 2, 3},
+    {5, 4, 2, 2, 4}, {5, 4, 4, 1, 3}, {5, 2, 2, 2, 4}, {2, 4, 2, 2, 4},
+};
+constexpr int kTileKinds = sizeof(kTiles) / sizeof(kTiles[0]);
+constexpr int tile_bm(int k) { return 16 * kTiles[k].wtm * kTiles[k].wm; }
+constexpr int tile_bn(int k) { return 16 * kTiles[k].wtn * kTiles[k].wn; }
+constexpr int tile_threads(int k) { return 64 * kTiles[k].wm * kTiles[k].wn; }
+
+constexpr int kGemmBK = 128;   // bytes (= E4M3 elements) of K per step
+
+// Split-K reductions.  kReduceKernel: fp32 partial tiles [splits][M][ldp] go
+// to the workspace and a second kernel adds them in split order.
+// kReduceLast: every workgroup of a split tile stores its partial tile, and
+// the last of them to arrive (an atomic ticket per tile) adds all of them in
+// split order and writes the output.  The tickets live in the first
+// kGemmTicketBytes of the workspace, which must be zero before the first call
+// and which every call leaves zero again.
+enum GemmReduce { kReduceNone = 0, kReduceKernel = 1, kReduceLast = 2 };
+constexpr size_t kGemmTicketBytes = 16384;   // 4096 tile tickets
+
+// ---- acceptance ---------------------------------------------------------------
+constexpr int kAcceptThreads = 256;
+constexpr int kAcceptVecs = 8;                                           // 16-byte vectors per lane per item
+constexpr int64_t kAcceptSlice = (int64_t)64 * kAcceptVecs * 8;          // 4096 logits per wave item
+constexpr int kAcceptPerThread = kAcceptVecs * 8;                        // 64 logits per thread (sampling)
+constexpr int64_t kAcceptChunk = (int64_t)kAcceptThreads * kAcceptPerThread;   // 16384 logits per sampling block
+
+}  // namespace specfp8

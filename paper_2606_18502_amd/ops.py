@@ -205,7 +205,7 @@ def gemm(a: torch.Tensor, sa: torch.Tensor, w: torch.Tensor, sw: torch.Tensor,
     ws_ptr, ws_bytes = None, 0
     if need:
         if workspace is None or workspace.numel() * workspace.element_size() < need:
-            workspace = torch.empty((need,), dtype=torch.uint8, device=a.device)
+            workspace = torch.zeros((need,), dtype=torch.uint8, device=a.device)   # tickets start at zero
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
     check("spec_fp8_gemm", lib.spec_fp8_gemm(a.data_ptr(), _rowmajor(a, "a"), sa.data_ptr(), a_mode,
                                              w.data_ptr(), _rowmajor(w, "w"), sw.data_ptr(), w_mode, M, N, K,

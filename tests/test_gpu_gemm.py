@@ -283,3 +283,26 @@ def test_elementwise_error_is_the_matrix_cores(M, N, K):
     ours, vendor = _report_elementwise(f"M={M} N={N} K={K}", y32, y_ref, da, dw, sa, sw)
     if vendor is not None:
         assert ours <= 2.0 * vendor + 1e-4, (ours, vendor)
+
+
+def test_split_workspace_reused_across_shapes():
+    """One zero-filled workspace serves split-K GEMMs of different shapes in
+    a row (the verify step's O and down projections, whose partial tiles the
+    last workgroup of each tile adds): every call leaves the ticket words
+    zero, and each result equals the same call on a fresh workspace, bit for
+    bit."""
+    p = need_gpu()
+    shapes = [(320, 4096, 4096), (320, 4096, 14336), (100, 4096, 1024), (320, 4096, 4096)]
+    need = max(p.gemm_workspace_bytes(M, N, K) for M, N, K in shapes)
+    assert all(p.gemm_workspace_bytes(M, N, K) > 0 for M, N, K in shapes)
+    ws = torch.zeros((need,), dtype=torch.uint8, device="cuda")
+    for i, (M, N, K) in enumerate(shapes):
+        say(f"shared workspace M={M} N={N} K={K}")
+        a, sa, w, sw = _operands(M, N, K, seed=100 + i, outliers=False)
+        args = (dev_u8(a), dev_f32(sa), dev_u8(w), dev_f32(sw))
+        y_shared = host(p.gemm(*args, out_dtype=torch.float32, workspace=ws))
+        assert np.all(host(ws[:16384]) == 0)
+        y_fresh = host(p.gemm(*args, out_dtype=torch.float32))
+        np.testing.assert_array_equal(y_shared, y_fresh)
+        if i == 0:
+            assert og.rel_error(y_shared, og.gemm(a, sa, w, sw)) <= TOL

@@ -40,7 +40,7 @@ def test_graph_replays_match_eager():
     q2 = torch.empty((M, K2), dtype=torch.uint8, device=dev)
     s2 = torch.empty((M,), dtype=torch.float32, device=dev)
     y2 = torch.empty((M, N2), dtype=torch.float32, device=dev)
-    gws = torch.empty((max(p.gemm_workspace_bytes(M, N1, K1), p.gemm_workspace_bytes(M, N2, K2), 16),),
+    gws = torch.zeros((max(p.gemm_workspace_bytes(M, N1, K1), p.gemm_workspace_bytes(M, N2, K2), 16),),
                       dtype=torch.uint8, device=dev)
     assert p.gemm_workspace_bytes(M, N2, K2) > 0       # the down shape splits K
     aws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device=dev)
