@@ -44,7 +44,13 @@ def load() -> ctypes.CDLL:
         return _lib
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_18502_amd.build`")
-    lib = ctypes.CDLL(LIB_PATH)
+    _lib = declare(ctypes.CDLL(LIB_PATH))
+    return _lib
+
+
+def declare(lib: ctypes.CDLL) -> ctypes.CDLL:
+    """Set the argument and result types of every entry point on a loaded
+    library that exports the C ABI."""
     i64, vp, f32, sz, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_size_t, ctypes.c_int
     lib.spec_fp8_quantize.argtypes = [vp, i64, i64, i64, i32, i32, vp, vp, i64, vp]
     lib.spec_fp8_quantize.restype = i32
@@ -85,7 +91,6 @@ def load() -> ctypes.CDLL:
     lib.spec_last_hip_error.restype = i32
     lib.spec_version.argtypes = []
     lib.spec_version.restype = i32
-    _lib = lib
     return lib
 
 

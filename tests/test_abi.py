@@ -19,6 +19,10 @@ A1 = 0x10001             # misaligned
 @pytest.fixture(scope="module")
 def lib():
     import paper_2606_18502_amd as p
+    san = os.environ.get("SPECFP8_ABI_LIB")
+    if san:            # the host-only build under sanitizers (tests/test_host_sanitizers.py)
+        from paper_2606_18502_amd import _lib
+        return _lib.declare(ctypes.CDLL(san))
     if not os.path.exists(p.LIB_PATH):
         from paper_2606_18502_amd import build
         build.build()
