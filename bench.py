@@ -843,9 +843,38 @@ def profile_gemm_c5(torch, p, wl):
     return 0
 
 
-def profile_accept_c4(torch, p, wl, reps=20):
+def profile_gemm_c3(torch, p, wl, rounds=10, copies=3):
+    """Kernels for kernel-trace and counter runs of the verify step's four
+    GEMMs at M = 320 (QKV, O, gate|up, down) in the step's launch
+    configuration: `rounds` rounds over `copies` weight copies, so each launch
+    finds its weights cold (3 copies of 218 MB exceed the 256 MB Infinity
+    Cache).  Every shape runs a kernel of its own, so a trace's per-kernel
+    averages are per-shape figures."""
+    cfg3 = wl.CONFIGS["C3"]
+    M = cfg3["M"]
+    lin = {n: (N, K) for n, N, K in cfg3["linears"]}
+    a = {n: torch.randint(0, 120, (M, K), dtype=torch.uint8, device="cuda") for n, (N, K) in lin.items()}
+    sa = torch.rand(M, device="cuda") * 0.01 + 1e-3
+    ws = [{n: torch.randint(0, 120, (N, K), dtype=torch.uint8, device="cuda") for n, (N, K) in lin.items()}
+          for _ in range(copies)]
+    sw = {n: torch.rand(N, device="cuda") * 0.01 + 1e-3 for n, (N, K) in lin.items()}
+    out = {n: torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for n, (N, K) in lin.items()}
+    wsb = torch.zeros((max(16, max(p.gemm_workspace_bytes(M, N, K) for N, K in lin.values())),),
+                      dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    for r in range(rounds):
+        for n in ("qkv", "o", "gate_up", "down"):
+            p.gemm(a[n], sa, ws[r % copies][n], sw[n], out=out[n], workspace=wsb)
+    torch.cuda.synchronize()
+    log("profile kernels done")
+    return 0
+
+
+def profile_accept_c4(torch, p, wl, reps=20, copies=3):
     """Kernels for a kernel-trace run of the acceptance alone: `reps` stochastic
-    (T = 0.7) and `reps` greedy acceptances of the C4 logits, back to back."""
+    (T = 0.7) and `reps` greedy acceptances of the C4 logits, back to back,
+    rotating over `copies` copies of the logits (3 x 147.75 MB exceed the
+    256 MB Infinity Cache, so every launch reads them cold)."""
     c = wl.CONFIGS["C4"]
     B, k, V, T = c["B"], c["k"], c["V"], c["temperature"]
     zt, zd = wl.accept_logits(B, k, V, c["seed"], wl.C4_CORRELATION, scale=c["logit_std"], rank=c["rank"])
@@ -857,12 +886,14 @@ def profile_accept_c4(torch, p, wl, reps=20):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to("cuda")
 
     dzt, dzd = dev(zt), dev(zd)
+    zts = [dzt] + [dzt.clone() for _ in range(copies - 1)]
+    zds = [dzd] + [dzd.clone() for _ in range(copies - 1)]
     dx, dxg, du = (torch.from_numpy(a).to("cuda") for a in (x, xg, u))
     ws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device="cuda")
-    for _ in range(reps):
-        p.verify_accept(dzt, dzd, dx, du, T, workspace=ws)
-    for _ in range(reps):
-        p.verify_accept(dzt, None, dxg, None, 0.0, workspace=ws)
+    for r in range(reps):
+        p.verify_accept(zts[r % copies], zds[r % copies], dx, du, T, workspace=ws)
+    for r in range(reps):
+        p.verify_accept(zts[r % copies], None, dxg, None, 0.0, workspace=ws)
     torch.cuda.synchronize()
     log("profile kernels done")
     return 0
@@ -875,11 +906,15 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--copies", type=int, default=3, help="rotated copies of weights and logits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "accept_c4"], default=None,
-                    help="for hardware-counter runs: 'traffic' = a plain copy of 256 MiB (the counters' "
+    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "gemm_c3", "accept_c4"], default=None,
+                    help="for profiler runs: 'traffic' = a plain copy of 256 MiB (the counters' "
                          "calibration), then 3 launches of the gate|up GEMM; 'gemm_c5' = 3 launches of the "
-                         "M=4096 4096->14336 GEMM; 'accept_c4' = 20 stochastic and 20 greedy acceptances of the "
-                         "C4 logits; then exit")
+                         "M=4096 4096->14336 GEMM; 'gemm_c3' = the four M=320 verify-step GEMMs, 10 rounds over "
+                         "3 rotated weight copies; 'accept_c4' = 20 stochastic and 20 greedy acceptances of the "
+                         "C4 logits over 3 rotated copies; then exit")
+    ap.add_argument("--part", choices=["gemm", "accept", "quantize"], default=None,
+                    help="time one part of the step only (cold, as in the full run) and print its figures "
+                         "as one JSON line")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}): the verify path runs on one "
@@ -906,8 +941,22 @@ def main(argv=None):
         return profile_gemm_c5(torch, p, wl)
     if args.profile == "accept_c4":
         return profile_accept_c4(torch, p, wl)
+    if args.profile == "gemm_c3":
+        return profile_gemm_c3(torch, p, wl)
     acts, weights, logits = build_inputs(torch, p, wl, args.copies)
     step = Step(torch, p, wl, acts)
+    if args.part is not None:
+        step.run(weights[0], logits[0])
+        torch.cuda.synchronize()
+        if args.part == "quantize":
+            out = quantize_parts(torch, p, wl, step)
+        else:
+            parts, spread = time_parts(torch, step, weights, logits, reps=42)
+            out = {"us": {n: round(v, 2) for n, v in parts.items()}, "p10_p90": spread}
+            if args.part == "accept":
+                out["greedy"] = greedy_accept_part(torch, p, step, logits)
+        print(json.dumps({"part": args.part, **out}), flush=True)
+        return 0
     cfg3, cfg4 = wl.CONFIGS["C3"], wl.CONFIGS["C4"]
     M = cfg3["M"]
     gemm_flops = sum(2.0 * M * N * K for _, N, K in cfg3["linears"])
