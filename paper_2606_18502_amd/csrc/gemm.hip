@@ -14,10 +14,11 @@
 //    global memory straight into LDS with global_load_lds_dwordx4 (no VGPR
 //    staging): one wave instruction moves 8 rows x 128 bytes = 1 KiB;
 //  * inside LDS each 128-byte row holds its eight 16-byte chunks in XOR-
-//    swizzled slots (slot = chunk ^ ((row >> 1) & 7), see swz); the swizzle is
-//    applied on the global side, so global reads stay fully coalesced, and the
-//    MFMA operand reads (ds_read_b128 of one logical chunk from 16
-//    consecutive rows) hit 16 distinct 16-byte bank groups -- no conflicts;
+//    swizzled slots (slot = chunk ^ swz(row)); the swizzle is applied on the
+//    global side, so global reads stay fully coalesced, and the MFMA operand
+//    reads (ds_read_b128, lane l reading logical chunk 2(l/16) + h of row
+//    l % 16) put the lanes that one LDS cycle serves on distinct banks -- no
+//    conflicts (see swz);
 //  * STAGES buffers rotate so that STAGES-1 K-steps of loads are in flight
 //    while the current one is multiplied.
 //
@@ -111,11 +112,17 @@ struct GemmCfg {
 };
 
 // LDS swizzle.  gfx950's LDS has 64 banks of 4 bytes (256 bytes per cycle),
-// so a ds_read_b128 serves 16 lanes per cycle.  Rows are 128 bytes, so rows
-// r and r^1 share a 256-byte bank line; placing logical chunk c of row r in
-// slot c ^ ((r >> 1) & 7) gives the 16 lanes that read one logical chunk of
-// 16 consecutive rows 16 different 16-byte bank groups.
-__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+// so a ds_read_b128 takes at least 4 cycles, 16 lanes per cycle; the lanes
+// served together are l and l + 16 for l % 16 < 8 (lanes 0-7 with 16-23,
+// 8-15 with 24-31, 32-39 with 48-55, 40-47 with 56-63): a control kernel
+// reading 16 contiguous bytes per lane counts no conflict, and the operand
+// read counted 4 conflict cycles of 8 under a swizzle that only kept lanes
+// 0-15 apart.  Rows are 128 bytes, so rows r and r^1 share a 256-byte bank
+// line (their chunks land in the two halves); lanes l and l + 16 read rows
+// 0-7 (or 8-15) at chunks differing by 2, so the XOR masks of the four row
+// pairs must form a set F with F and F ^ 2 disjoint: F = {0, 1, 4, 5}.  Every
+// cycle's 16 lanes then hit 16 different 16-byte bank groups.
+__device__ __forceinline__ int swz(int row) { return (0x5410 >> (4 * ((row >> 1) & 3))) & 0xf; }
 
 // Load group i (of kGroupsPerWave) of this wave for the stage at `stage`.
 template <class C>
