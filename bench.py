@@ -102,12 +102,18 @@ class Step:
         self.out = torch.empty((B, k + 1), dtype=torch.int32, device=dev)
         self.num = torch.empty((B,), dtype=torch.int32, device=dev)
 
-    def run(self, weights, logits):
+    def run(self, weights, logits, gate_up_events=None):
+        """One verify step.  `gate_up_events` (a pair of timing events) are
+        recorded on the current stream around the gate|up GEMM."""
         p = self.p
         for name in ("qkv", "o", "gate_up"):
             p.quantize(self.acts[name], out=self.q[name], scales=self.s[name])
             w, sw = weights[name]
+            if name == "gate_up" and gate_up_events is not None:
+                gate_up_events[0].record()
             p.gemm(self.q[name], self.s[name], w, sw, out=self.y[name], workspace=self.gws)
+            if name == "gate_up" and gate_up_events is not None:
+                gate_up_events[1].record()
         p.quantize(self.y["gate_up"], silu_mul=True, out=self.q["down"], scales=self.s["down"])
         w, sw = weights["down"]
         p.gemm(self.q["down"], self.s["down"], w, sw, out=self.y["down"], workspace=self.gws)
@@ -119,13 +125,14 @@ def time_parts(torch, step, weights, logits, reps):
     """Per-part event timing: each part (one GEMM, or the acceptance) is
     launched `reps` times back to back on the current stream, every launch
     bracketed by HIP events, so the GPU never waits for the host between
-    them; returns the mean launch duration in us per part, and the 10th and
-    90th percentiles.  Cold: the weight and logit copies rotate, so a launch
+    them; the first two launches of each part are dropped.  Returns the mean
+    and the median launch duration in us per part, and the 10th and 90th
+    percentiles.  Cold: the weight and logit copies rotate, so a launch
     finds none of its bytes in the 256 MB Infinity Cache; gate_up_warm
     repeats one weight copy (the warm-cache figure, reported separately)."""
     p = step.p
     names = ["qkv", "o", "gate_up", "gate_up_warm", "gate_up_silu", "down", "accept"]
-    res, spread = {}, {}
+    res, med, spread = {}, {}, {}
     for n in names:
         evs = []
         for r in range(reps):
@@ -148,8 +155,9 @@ def time_parts(torch, step, weights, logits, reps):
         torch.cuda.synchronize()
         ts = np.array([a.elapsed_time(b) for a, b in evs[2:]]) * 1e3
         res[n] = float(np.mean(ts))
+        med[n] = round(float(np.median(ts)), 2)
         spread[n] = [round(float(np.percentile(ts, 10)), 1), round(float(np.percentile(ts, 90)), 1)]
-    return res, spread
+    return res, med, spread
 
 
 def vendor_gemm(torch, step, weights, reps=22):
@@ -906,12 +914,13 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--copies", type=int, default=3, help="rotated copies of weights and logits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "gemm_c3", "accept_c4"], default=None,
+    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "gemm_c3", "accept_c4", "step"], default=None,
                     help="for profiler runs: 'traffic' = a plain copy of 256 MiB (the counters' "
                          "calibration), then 3 launches of the gate|up GEMM; 'gemm_c5' = 3 launches of the "
                          "M=4096 4096->14336 GEMM; 'gemm_c3' = the four M=320 verify-step GEMMs, 10 rounds over "
                          "3 rotated weight copies; 'accept_c4' = 20 stochastic and 20 greedy acceptances of the "
-                         "C4 logits over 3 rotated copies; then exit")
+                         "C4 logits over 3 rotated copies; 'step' = --warmup and then --steps eager verify "
+                         "steps over the rotated copies, nothing else; then exit")
     ap.add_argument("--part", choices=["gemm", "accept", "quantize"], default=None,
                     help="time one part of the step only (cold, as in the full run) and print its figures "
                          "as one JSON line")
@@ -945,14 +954,21 @@ def main(argv=None):
         return profile_gemm_c3(torch, p, wl)
     acts, weights, logits = build_inputs(torch, p, wl, args.copies)
     step = Step(torch, p, wl, acts)
+    if args.profile == "step":
+        # the benched step alone, so a kernel trace holds its launches only
+        for i in range(args.warmup + args.steps):
+            step.run(weights[i % args.copies], logits[i % args.copies])
+        torch.cuda.synchronize()
+        log(f"profile step done: {args.warmup} + {args.steps} steps")
+        return 0
     if args.part is not None:
         step.run(weights[0], logits[0])
         torch.cuda.synchronize()
         if args.part == "quantize":
             out = quantize_parts(torch, p, wl, step)
         else:
-            parts, spread = time_parts(torch, step, weights, logits, reps=42)
-            out = {"us": {n: round(v, 2) for n, v in parts.items()}, "p10_p90": spread}
+            parts, med, spread = time_parts(torch, step, weights, logits, reps=102)
+            out = {"us": {n: round(v, 2) for n, v in parts.items()}, "median_us": med, "p10_p90": spread}
             if args.part == "accept":
                 out["greedy"] = greedy_accept_part(torch, p, step, logits)
         print(json.dumps({"part": args.part, **out}), flush=True)
@@ -978,16 +994,21 @@ def main(argv=None):
     torch.cuda.synchronize()
     log("warmup done")
 
-    # timed region: K eager steps (launches queue ahead of the GPU)
+    # timed region: K eager steps (launches queue ahead of the GPU); the
+    # dominant kernel (gate|up) is bracketed by events on its stream in every
+    # step, so the roofline's launch duration is measured in the step itself
     torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
+    gu_events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in range(args.steps)]
     t_start.record()
     for i in range(args.steps):
-        step.run(weights[i % args.copies], logits[i % args.copies])
+        step.run(weights[i % args.copies], logits[i % args.copies], gate_up_events=gu_events[i])
     t_end.record()
     torch.cuda.synchronize()
     ms_step = t_start.elapsed_time(t_end) / args.steps
+    gu_step_us = np.array([a.elapsed_time(b) for a, b in gu_events]) * 1e3
     num = step.num.cpu().numpy()
     tokens = float(np.sum(num + 1))
 
@@ -1000,7 +1021,7 @@ def main(argv=None):
     torch.cuda.synchronize()
     ms_step_graph = e0.elapsed_time(e1) / args.steps
 
-    parts, spread = time_parts(torch, step, weights, logits, reps=22)
+    parts, med, spread = time_parts(torch, step, weights, logits, reps=102)
     vendor = vendor_gemm(torch, step, weights)
     lm = lm_head_parts(torch, p, wl)
     tree = tree_parts(torch, p, wl)
@@ -1018,7 +1039,7 @@ def main(argv=None):
     log(f"LM head: gemm {lm['gemm']} us (with statistics {lm['gemm_with_stats']}); accept {lm['accept']} us "
         f"(from statistics {lm['accept_from_stats']}); unfused {lm['unfused_us']} us, fused {lm['fused_us']} us")
     gemm_us = parts["qkv"] + parts["o"] + parts["gate_up"] + parts["down"]
-    gu_us, acc_us = parts["gate_up"], parts["accept"]
+    gu_us, acc_us = float(np.mean(gu_step_us)), parts["accept"]
     log(f"step {ms_step * 1e3:.1f} us (eager), {ms_step_graph * 1e3:.1f} us (graph); gate_up gemm {gu_us:.1f} us; "
         f"accept {acc_us:.1f} us")
 
@@ -1047,6 +1068,7 @@ def main(argv=None):
             "gemm_us": {n: round(parts[n], 1) for n in ("qkv", "o", "gate_up", "gate_up_silu", "down")},
             "gate_up_warm_cache_us": round(parts["gate_up_warm"], 1),
             "hipblaslt_gemm_us": vendor,
+            "part_us_median": med,
             "part_us_p10_p90": spread,
             "lm_head_and_accept_us": lm,
             "tree_accept": tree,
@@ -1077,6 +1099,8 @@ def main(argv=None):
             "traffic": measured_traffic(),
             "algorithmic_bytes": gu_bytes,
             "avg_launch_us": round(gu_us, 2),
+            "launch_us_source": f"HIP events around the gate|up launch in each of the {args.steps} timed steps "
+                                f"(median {np.median(gu_step_us):.2f} us)",
             "mfma_frac": round(gu_flops / (gu_us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 3),
         },
     }

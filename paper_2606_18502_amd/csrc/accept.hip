@@ -32,6 +32,7 @@
 // position where sampling happens (<= 2 rows per sequence), with every load of
 // a thread issued before it computes.  All reductions use a fixed order, so
 // results are deterministic.
+#include <atomic>
 #include <mutex>
 
 #include "device_common.hpp"
@@ -57,7 +58,6 @@ constexpr int64_t kChunk = kAcceptChunk;               // 16384 logits per sampl
 static_assert(kSlice == (int64_t)kWave * kVecs * 8 && kChunk == (int64_t)kAThreads * kPerThread, "accept geometry");
 constexpr int kMaxChunks = kAThreads;                 // V <= 2^22: one chunk per thread
 constexpr int kStreamWavesPerCU = 12;
-constexpr int kCUs = 256;
 
 struct AcceptArgs {
     const uint16_t* zt;
@@ -142,12 +142,12 @@ __device__ __forceinline__ void vals8(const uint16_t* __restrict__ row, const ui
 // holding one workgroup more than its neighbours sets the kernel's end
 // (measured on the C4 workload: 3.6 workgroups per CU 27.9 us, exactly 3 per
 // CU 25.8 us).  Waves past the last item return at once.
-inline unsigned stream_blocks(int64_t items) {
-    const int64_t cap = (int64_t)kCUs * kStreamWavesPerCU;
+inline unsigned stream_blocks(int64_t items, int cus) {
+    const int64_t cap = (int64_t)cus * kStreamWavesPerCU;
     const int64_t per = (items + cap - 1) / cap;
     const int64_t waves = (items + per - 1) / per;
     int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
-    if (blocks > kCUs) blocks = (blocks + kCUs - 1) / kCUs * kCUs;
+    if (blocks > cus) blocks = (blocks + cus - 1) / cus * cus;
     return (unsigned)blocks;
 }
 
@@ -1039,6 +1039,25 @@ __global__ __launch_bounds__(256) void clear_tickets_kernel(unsigned int* ctr, i
 constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mutex;
 void* g_scratch_ptr[kMaxDevices] = {};
+std::atomic<int> g_cus[kMaxDevices];
+
+// Compute units of the current device (256 on MI355X), looked up once per
+// device; the streaming grids are sized from it.
+hipError_t device_cus(int* cus) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    int n = g_cus[dev].load(std::memory_order_relaxed);
+    if (n <= 0) {
+        e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        if (n <= 0) return hipErrorInvalidDevice;
+        g_cus[dev].store(n, std::memory_order_relaxed);
+    }
+    *cus = n;
+    return hipSuccess;
+}
 
 }  // namespace
 
@@ -1063,6 +1082,8 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
                          const float* u, int64_t B, int64_t k, int64_t V, float temperature,
                          int32_t* out_tokens, int32_t* num_accepted, void* workspace, hipStream_t stream,
                          const float2* tstats, int64_t n_tstats, int64_t ld_tstats) {
+    int cus = 0;
+    if (hipError_t e = device_cus(&cus); e != hipSuccess) return e;
     AcceptArgs a{};
     a.tst = tstats; a.ntst = (uint32_t)n_tstats; a.ldtst = ld_tstats;
     char* ws = reinterpret_cast<char*>(workspace);
@@ -1080,7 +1101,7 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
         a.c2 = 0.0f;
         a.items = (uint32_t)(B * a.Rs * p.nschunk);
         if (a.items > 0) {
-            const unsigned g1 = stream_blocks(a.items);
+            const unsigned g1 = stream_blocks(a.items, cus);
             if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
             else hipLaunchKernelGGL(greedy_partial_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
             hipError_t e = hipGetLastError();
@@ -1094,7 +1115,7 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
     a.c2 = (float)(1.4426950408889634 / (double)temperature);
     a.items = (uint32_t)(B * a.Rs * p.nschunk);
     if (a.items > 0) {
-        const unsigned g1 = stream_blocks(a.items);
+        const unsigned g1 = stream_blocks(a.items, cus);
         if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
         else hipLaunchKernelGGL(stoch_stats_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
     } else {
@@ -1113,6 +1134,8 @@ hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int
                               const float* u, int64_t B, int64_t N, int64_t V, float temperature,
                               int32_t* out_tokens, int32_t* accepted_nodes, int32_t* num_accepted, void* workspace,
                               hipStream_t stream) {
+    int cus = 0;
+    if (hipError_t e = device_cus(&cus); e != hipSuccess) return e;
     AcceptArgs a{};
     char* ws = reinterpret_cast<char*>(workspace);
     a.zt = zt; a.zd = nullptr; a.x = x; a.u = u; a.out = out_tokens; a.num = num_accepted;
@@ -1127,7 +1150,7 @@ hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int
     a.rt0 = 0;
     a.items = (uint32_t)(B * a.Rs * p.nschunk);
     const bool vec = (V % 8 == 0) && ((uintptr_t)zt % 16 == 0);
-    const unsigned g1 = stream_blocks(a.items);
+    const unsigned g1 = stream_blocks(a.items, cus);
     if (temperature == 0.0f) {
         a.c2 = 0.0f;
         if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
