@@ -40,6 +40,8 @@
 //     whose 16-row blocks pair 8 gate rows with the matching 8 up rows.
 #include <float.h>
 
+#include <utility>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 #include "plan.hpp"
@@ -718,6 +720,239 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g) {
     }
 }
 
+// ---- long prompts: 256-wide tiles, operand fragments refilled in place ------
+//
+// At large M every CU runs several tiles, and its time follows the operand
+// bytes it streams (its data path, not its matrix cores, sets the pace).  A
+// 256x224 or 256x256 tile (2x2 waves of 128x112 or 128x128) streams 22-27%
+// fewer operand bytes per output than 160x224.  Its 224-256 accumulators per
+// lane leave no room for a second set of operand fragments, so each fragment
+// is refilled with the next K-step's data as soon as its last MFMA of the
+// current step has issued: the MFMAs run W-block-major, so a W fragment dies
+// after its WTM MFMAs and the A fragments during the last W block.  Two LDS
+// stages (60 or 64 KiB): the loads of step it+2 go out while step it
+// multiplies.  The loads take the uniform-base form: the K-step's base
+// addresses are scalars and each lane keeps one 32-bit offset per load group
+// for the whole K loop (the plan takes this kernel only when M * lda and
+// N * ldw fit in 32 bits).
+constexpr int kRollDelay = 2;   // MFMAs between a fragment's last use and its refill
+
+template <int WTM, int WTN>
+struct RollCfg {
+    static constexpr int kThreads = 256;                  // 2 x 2 waves
+    static constexpr int BM = 32 * WTM;
+    static constexpr int BN = 32 * WTN;
+    static constexpr int kRows = BM + BN;
+    static constexpr int kGroupsPerWave = kRows / 32;     // 8-row (1 KiB) load groups per wave and stage
+    static constexpr int kStageBytes = kRows * kBK;
+    // group q of wave w covers rows 8 (w + 4 q) ..: activation rows for q < WTM
+    static_assert(BM / 8 == 4 * WTM, "the first WTM groups of every wave load A");
+};
+
+// Load group q of this wave for a stage: the group's 8 rows x 128 bytes go
+// from base + off (base: the K-step's first byte of A or W, a scalar; off:
+// this lane's row and chunk) to LDS at m0 = the group's 1 KiB.  Written as
+// inline asm to get the scalar-base form; the issuing code waits for it with
+// explicit vmcnt waits.
+__device__ __forceinline__ void roll_load(const uint8_t* base, uint32_t off, uint32_t lds) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
+}
+
+// ds_read_b128 at vaddr + OFF (OFF < 64 KiB, an immediate).
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read_imm(uint32_t vaddr) {
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(vaddr), "n"(OFF));
+    return v;
+}
+
+// The 16x16 operand block b (16 rows from the wave's first row of A or W, plus
+// 16 b) of this lane: row r16 = lane % 16 of the block, logical chunks
+// 2 kg, 2 kg + 1 (kg = lane / 16).  All blocks of a wave share the row bits
+// that decide the swizzle, so each lane's two addresses are fixed per stage
+// (base[0], base[1]) and the block is an immediate offset of 16 rows x 128.
+template <int B>
+__device__ __forceinline__ v8i roll_frag(const uint32_t (&base)[2]) {
+    const u32x4 lo = lds_read_imm<B * 2048>(base[0]);
+    const u32x4 hi = lds_read_imm<B * 2048>(base[1]);
+    return __builtin_bit_cast(v8i, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+template <int WTM, int WTN, int N>
+struct RollRead {
+    // fragment N of the step order: W blocks 0 .. WTN-1, then A blocks
+    __device__ __forceinline__ static void run(Frags<WTM, WTN>& f, const uint32_t (&wb)[2], const uint32_t (&ab)[2]) {
+        if constexpr (N < WTN) f.w[N] = roll_frag<N>(wb);
+        else f.a[N - WTN] = roll_frag<N - WTN>(ab);
+    }
+};
+
+// f(std::integral_constant<int, I>{}) for I = 0 .. N-1, in order, each I a
+// compile-time constant (an immediate LDS offset, a fragment index).
+template <class F, int... I>
+__device__ __forceinline__ void static_for_seq(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// One K-step `it` on stage S.  LOADS: refill stage S with step it+2 (there is
+// one); NEXT: refill the fragments with step it+1 (there is one).  ab/wb: this
+// lane's A and W read bases in stage S ^ 1.
+template <class R, int WTM, int WTN, int S, bool LOADS, bool NEXT>
+__device__ __forceinline__ void roll_step(const GemmArgs& g, int it, int nk, int krot,
+                                          const uint32_t (&off)[R::kGroupsPerWave], uint32_t lds_stage,
+                                          const uint32_t (&ab)[2], const uint32_t (&wb)[2], v4f (&acc)[WTN][WTM],
+                                          Frags<WTM, WTN>& f) {
+    wait_vmcnt<0>();                      // step it+1 has landed (this wave's loads) ...
+    __builtin_amdgcn_s_barrier();         // ... and every wave's; every wave has read step it from stage S
+    const int64_t kref = (int64_t)((it + 2 + krot) % nk) * kBK;
+    const uint8_t* abase = g.a + kref;
+    const uint8_t* wbase = g.w + kref;
+    constexpr int kMfma = WTM * WTN;
+    constexpr int kG = R::kGroupsPerWave;
+    constexpr int kLSpan = (kMfma * kLoadSpan8 + 7) / 8;
+    // refill order: W block i after its last MFMA (i WTM + WTM - 1), A block j
+    // after its last one ((WTN - 1) WTM + j), each kRollDelay MFMAs later
+    auto refill = [&](auto td_c) {
+        constexpr int td = decltype(td_c)::value;
+        if constexpr (td % WTM == WTM - 1 && td / WTM < WTN - 1) RollRead<WTM, WTN, td / WTM>::run(f, wb, ab);
+        if constexpr (td >= (WTN - 1) * WTM) RollRead<WTM, WTN, WTN + td - (WTN - 1) * WTM>::run(f, wb, ab);
+    };
+    static_for<kMfma>([&](auto tc) {
+        constexpr int t = decltype(tc)::value;
+        constexpr int i = t / WTM, j = t % WTM;
+        if constexpr (LOADS) {
+            static_for<kG>([&](auto qc) {
+                constexpr int q = decltype(qc)::value;
+                if constexpr ((q * kLSpan) / kG == t) roll_load(q < WTM ? abase : wbase, off[q], lds_stage + q * 4096);
+            });
+        }
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(f.w[i], f.a[j], acc[i][j], 0, 0, 0, 0, 0, 0);
+        if constexpr (NEXT && t >= kRollDelay) refill(std::integral_constant<int, t - kRollDelay>{});
+        __builtin_amdgcn_sched_barrier(0);
+    });
+    if constexpr (NEXT) {
+        // the fragments whose last MFMAs issued just now (wait states first,
+        // so that those MFMAs have read their operands)
+        asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+        static_for<kRollDelay>([&](auto dc) { refill(std::integral_constant<int, kMfma - kRollDelay + decltype(dc)::value>{}); });
+        RollRead<WTM, WTN, WTN - 1>::run(f, wb, ab);
+        lds_wait_all();
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) asm volatile("" : "+v"(f.a[j]));
+#pragma unroll
+        for (int i = 0; i < WTN; ++i) asm volatile("" : "+v"(f.w[i]));
+    }
+}
+
+template <int WTM, int WTN>
+__global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
+    using R = RollCfg<WTM, WTN>;
+    __shared__ __attribute__((aligned(1024))) char lds0[R::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) char lds1[R::kStageBytes];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % 2;
+    const int wn = wave / 2;
+
+    const int total = g.m_tiles * g.n_tiles;
+    const int tile = xcd_remap(blockIdx.x, total);
+    int mt, nt;
+    if (g.group_m > 1) {
+        const int per_group = g.group_m * g.n_tiles;
+        const int first = (tile / per_group) * g.group_m;
+        const int gm = min(g.group_m, g.m_tiles - first);
+        const int in = tile - (tile / per_group) * per_group;
+        mt = first + in % gm;
+        nt = in / gm;
+    } else {
+        mt = tile % g.m_tiles;
+        nt = tile / g.m_tiles;
+    }
+    const int m0 = mt * R::BM;
+    const int n0 = nt * R::BN;
+    const int nk = g.ksteps;
+    const int krot = g.krot_on ? (nt * 7) % nk : 0;
+
+    // per-lane offsets of the load groups (rows past the edge re-read the last row)
+    uint32_t off[R::kGroupsPerWave];
+#pragma unroll
+    for (int q = 0; q < R::kGroupsPerWave; ++q) {
+        const int row = (wave + 4 * q) * 8 + (lane >> 3);
+        const int chunk = (lane & 7) ^ swz(row);
+        if (q < WTM) {
+            const int m = min(m0 + row, g.M - 1);
+            off[q] = (uint32_t)m * (uint32_t)g.lda + (uint32_t)(chunk * 16);
+        } else {
+            const int n = min(n0 + row - R::BM, g.N - 1);
+            off[q] = (uint32_t)n * (uint32_t)g.ldw + (uint32_t)(chunk * 16);
+        }
+    }
+    // LDS: the group's 1 KiB of each stage (m0 of the loads), and this lane's
+    // operand read bases in each stage
+    const uint32_t st[2] = {lds_addr(lds0), lds_addr(lds1)};
+    const uint32_t ld0 = st[0] + (uint32_t)wave * 1024, ld1 = st[1] + (uint32_t)wave * 1024;
+    const int kg = lane >> 4, r16 = lane & 15;
+    uint32_t ab[2][2], wb[2][2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const uint32_t in_row = (uint32_t)(r16 * kBK + (((2 * kg + h) ^ swz(r16)) << 4));
+            ab[s][h] = st[s] + (uint32_t)(wm * WTM * 16 * kBK) + in_row;
+            wb[s][h] = st[s] + (uint32_t)((R::BM + wn * WTN * 16) * kBK) + in_row;
+        }
+
+    v4f acc[WTN][WTM];
+#pragma unroll
+    for (int i = 0; i < WTN; ++i)
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    // prologue: steps 0 and 1 in flight, then the fragments of step 0
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        const int64_t kb = (int64_t)((min(s, nk - 1) + krot) % nk) * kBK;
+#pragma unroll
+        for (int q = 0; q < R::kGroupsPerWave; ++q)
+            roll_load(q < WTM ? g.a + kb : g.w + kb, off[q], (s ? ld1 : ld0) + q * 4096);
+    }
+    wait_vmcnt<R::kGroupsPerWave>();
+    __builtin_amdgcn_s_barrier();
+    Frags<WTM, WTN> f;
+    static_for<WTM + WTN>([&](auto nc) { RollRead<WTM, WTN, decltype(nc)::value>::run(f, wb[0], ab[0]); });
+    lds_wait_all();
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) asm volatile("" : "+v"(f.a[j]));
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) asm volatile("" : "+v"(f.w[i]));
+
+    // steady state in pairs of steps (stage 0, stage 1) that both refill
+    // their stage, then the last pair (the plan takes this kernel only for an
+    // even number of K-steps), so no step is behind a branch
+#define SPEC_ROLL(S, LOADS, NEXT, IT) \
+    roll_step<R, WTM, WTN, S, LOADS, NEXT>(g, IT, nk, krot, off, S ? ld1 : ld0, ab[S ^ 1], wb[S ^ 1], acc, f)
+    for (int it = 0; it + 2 < nk; it += 2) {
+        SPEC_ROLL(0, true, true, it);
+        SPEC_ROLL(1, true, true, it + 1);
+    }
+    SPEC_ROLL(0, false, true, nk - 2);
+    SPEC_ROLL(1, false, false, nk - 1);
+#undef SPEC_ROLL
+    wait_vmcnt<0>();
+
+    float sa_reg[WTM];
+    float sw_reg[WTN][4];
+    load_scales<WTM, WTN>(g, sa_reg, sw_reg, m0, n0, wm, wn, lane);
+    store_tile<WTM, WTN, 2, 0>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, 0, nt, R::BM, R::BN);
+}
+
 // ---- tile configurations (plan.hpp, kTiles) ----------------------------------
 
 // The statistics epilogues are separate instantiations, so the plain GEMMs'
@@ -754,6 +989,18 @@ hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
     return hipGetLastError();
 }
 
+template <int KIND>
+hipError_t launch_roll(const GemmArgs& g, hipStream_t stream) {
+    constexpr int WTM = kTiles[KIND].wtm, WTN = kTiles[KIND].wtn;
+    static_assert(kTiles[KIND].roll && kTiles[KIND].wm == 2 && kTiles[KIND].wn == 2 && kTiles[KIND].stages == 2,
+                  "roll tiles are 2x2 waves over 2 stages");
+    static_assert(RollCfg<WTM, WTN>::BM == tile_bm(KIND) && RollCfg<WTM, WTN>::BN == tile_bn(KIND), "tile table");
+    if (g.splits != 1 || g.stats_mode != 0 || g.silu_inter != 0 || g.ksteps < 2 || g.ksteps % 2 != 0)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_fp8_roll_kernel<WTM, WTN>), dim3(g.m_tiles * g.n_tiles), dim3(256), 0, stream, g);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const float* sa, int a_per_tensor,
@@ -761,6 +1008,13 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
                        int64_t N, int64_t K, void* y, int64_t ldy, int out_f32, void* workspace,
                        hipStream_t stream, int stats_mode, float c2, float2* stats, int64_t ld_stats,
                        int64_t silu_inter) {
+    if (kTiles[p.kind].roll && ((uint64_t)(M - 1) * (uint64_t)lda + kBK > (1ull << 32) ||
+                                (uint64_t)(N - 1) * (uint64_t)ldw + kBK > (1ull << 32))) {
+        // its per-lane offsets are 32-bit: operands past 4 GiB take the 160x224 kernel
+        const GemmPlan q = plan_gemm_as(M, N, K, 2, 1, kReduceNone, kEpiPlain);
+        return launch_gemm(q, a, lda, sa, a_per_tensor, w, ldw, sw, w_per_tensor, M, N, K, y, ldy, out_f32,
+                           workspace, stream, stats_mode, c2, stats, ld_stats, silu_inter);
+    }
     GemmArgs g;
     g.stats = stats; g.ld_stats = ld_stats; g.stats_mode = stats_mode; g.c2 = c2;
     g.silu_inter = (int)silu_inter;
@@ -787,9 +1041,11 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
         case 6: e = launch_cfg<6>(g, stream); break;
         case 7: e = launch_cfg<7>(g, stream); break;
         case 8: e = launch_cfg<8>(g, stream); break;
+        case 9: e = launch_roll<9>(g, stream); break;
+        case 10: e = launch_roll<10>(g, stream); break;
         default: return hipErrorInvalidValue;
     }
-    static_assert(kTileKinds == 9, "every tile kind has a case");
+    static_assert(kTileKinds == 11, "every tile kind has a case");
     if (e != hipSuccess || p.splits == 1 || p.reduce != kReduceKernel) return e;
     const int64_t work = M * ((N + 3) / 4);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, stream, g);

@@ -19,6 +19,9 @@ GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int
     // the statistics epilogues never split K; the 160x224 tile has no
     // statistics variant (it would spill), 160x192 takes its place
     if (epilogue == kEpiStats && kind == 2) kind = 4;
+    // the in-place-refill kernels have the plain epilogue only and no K split
+    if (kTiles[kind].roll && epilogue != kEpiPlain) kind = epilogue == kEpiStats ? 4 : 2;
+    if (kTiles[kind].roll) splits = 1;
     if (epilogue != kEpiPlain) splits = 1;
     p.kind = kind;
     const int bm = tile_bm(kind), bn = tile_bn(kind);
@@ -96,7 +99,20 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
         if (N <= 4096) return plan_gemm_as(M, N, K, 7, 2, kReduceLast, epilogue);
         return plan_gemm_as(M, N, K, 8, 1, kReduceNone, epilogue);
     }
-    return plan_gemm_as(M, N, K, 2, 1, kReduceNone, epilogue);
+    // Long prompts.  A CU's time is its operand bytes: per tile (BM + BN)
+    // rows per K-step, times the rounds of tiles every CU runs.  The 256-wide
+    // in-place-refill tiles stream fewer rows per output; take the kind with
+    // the fewest rows per CU (an even number of K-steps is required by them).
+    int best = 2;
+    if (M >= 1024 && epilogue == kEpiPlain && ksteps >= 2 && ksteps % 2 == 0) {
+        auto cost = [&](int kind) {
+            const int64_t tiles = ((M + tile_bm(kind) - 1) / tile_bm(kind)) * ((N + tile_bn(kind) - 1) / tile_bn(kind));
+            return ((tiles + 255) / 256) * (int64_t)(tile_bm(kind) + tile_bn(kind));
+        };
+        for (int kind : {9, 10})
+            if (cost(kind) < cost(best)) best = kind;
+    }
+    return plan_gemm_as(M, N, K, best, 1, kReduceNone, epilogue);
 }
 
 AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {

@@ -9,9 +9,11 @@ namespace specfp8 {
 
 // ---- FP8 GEMM tiles ---------------------------------------------------------
 // A tile is a WM x WN grid of waves, each wave holding WTM x WTN blocks of
-// 16x16 outputs; STAGES LDS buffers rotate through the K-loop.
+// 16x16 outputs; STAGES LDS buffers rotate through the K-loop.  roll: the
+// long-prompt kernel whose operand fragments are refilled in place (one
+// fragment set; never split in K, plain epilogue only).
 struct TileShape {
-    int wtm, wtn, wm, wn, stages;
+    int wtm, wtn, wm, wn, stages, roll;
 };
 
 // kind  BM x BN   waves (wave tile)     stages  LDS      used for
@@ -24,9 +26,12 @@ struct TileShape {
 //  6   320 x 64   4x1 (80x64)           3       144 KiB
 //  7   160 x 64   2x2 (80x32)           4       112 KiB  M <= 320, N <= 4096 (split)
 //  8    64 x 128  2x2 (32x64)           4        96 KiB  M <= 64 wide N; M <= 320 short N
+//  9   256 x 224  2x2 (128x112), roll   2       120 KiB  large M
+// 10   256 x 256  2x2 (128x128), roll   2       128 KiB  large M
 constexpr TileShape kTiles[] = {
-    {2, 2, 2, 2, 4}, {5, 4, 1, 2, 4}, {5, 7, 2, 2, 3}, {8, 4, 2, 2, 3}, {5, 6, 2, 2, 3},
-    {5, 4, 2, 2, 4}, {5, 4, 4, 1, 3}, {5, 2, 2, 2, 4}, {2, 4, 2, 2, 4},
+    {2, 2, 2, 2, 4, 0}, {5, 4, 1, 2, 4, 0}, {5, 7, 2, 2, 3, 0}, {8, 4, 2, 2, 3, 0}, {5, 6, 2, 2, 3, 0},
+    {5, 4, 2, 2, 4, 0}, {5, 4, 4, 1, 3, 0}, {5, 2, 2, 2, 4, 0}, {2, 4, 2, 2, 4, 0}, {8, 7, 2, 2, 2, 1},
+    {8, 8, 2, 2, 2, 1},
 };
 constexpr int kTileKinds = sizeof(kTiles) / sizeof(kTiles[0]);
 constexpr int tile_bm(int k) { return 16 * kTiles[k].wtm * kTiles[k].wm; }

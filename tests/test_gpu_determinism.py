@@ -22,6 +22,7 @@ def _q(p, M, K, seed):
     (8, 1024, 512), (64, 4096, 4096), (80, 6144, 1024), (80, 28672, 512),   # small M, split K, wide N
     (320, 28672, 1024), (320, 4096, 4096), (320, 6144, 1024), (320, 4096, 2048),
     (1300, 672, 256),                                                         # grouped large-M order
+    (4096, 4096, 256), (2048, 7168, 512),                                     # 256x256, 256x224 in-place-refill tiles
     (300, 60096, 256),                                                        # 160x192 tiles, wide N
 ])
 def test_gemm_twice(M, N, K):

@@ -104,6 +104,46 @@ def test_gemm_parity(M, N, K):
     np.testing.assert_array_equal(y16, _f32_to_bf16_bits(y32))
 
 
+@pytest.mark.parametrize("M,N,K,out_f32,per_tensor,strided", [
+    # shapes the planner gives the long-prompt tiles whose fragments are
+    # refilled in place (fewer operand rows per CU than 160x224 tiles)
+    (4096, 4096, 256, True, False, False),    # 256x256, one tile per CU; two K-steps: no steady-state loop
+    (4000, 4000, 1024, True, False, True),    # 256x256, ragged M and N, strided operands and output
+    (2048, 7168, 512, False, False, False),   # 256x224, bf16 output
+    (2000, 7000, 512, True, True, True),      # 256x224, ragged, per-tensor activation scale, strided
+])
+def test_long_prompt_tiles(M, N, K, out_f32, per_tensor, strided):
+    """Random code bytes over the whole E4M3 range; sampled rows against the
+    oracle (tolerance and accumulation bound), the bf16 output against the
+    same kernel's fp32 output, and padding left untouched."""
+    p = need_gpu()
+    say(f"long-prompt gemm M={M} N={N} K={K} f32={out_f32} per_tensor={per_tensor} strided={strided}")
+    a = wl.fp8_code_bytes(M, K, seed=M + K)
+    w = wl.fp8_code_bytes(N, K, seed=N + K + 1)
+    sa = wl.uniform_scales(1, seed=M)[0] if per_tensor else wl.uniform_scales(M, seed=M)
+    sw = wl.uniform_scales(N, seed=N + 1)
+    pa, pw, py = (128, 256, 8) if strided else (0, 0, 0)
+    da = dev_u8(np.pad(a, ((0, 0), (0, pa))))[:, :K]
+    dw = dev_u8(np.pad(w, ((0, 0), (0, pw))))[:, :K]
+    dsa = dev_f32([sa] if per_tensor else sa)
+    dsw = dev_f32(sw)
+    rows, cols = _sample(M, 64, 3), _sample(N, 64, 4)
+    y_ref = og.gemm_rows(a, sa, w, sw, rows)
+    outs = {}
+    for dt in ([torch.float32, torch.bfloat16] if out_f32 else [torch.bfloat16, torch.float32]):
+        out = torch.full((M, N + py), -7.0, dtype=dt, device="cuda")
+        p.gemm(da, dsa, dw, dsw, out=out[:, :N])
+        o = host(out.float())
+        assert np.all(o[:, N:] == -7.0)
+        outs[dt] = (out, o[:, :N])
+    y32 = outs[torch.float32][1]
+    err = og.rel_error(y32[rows], y_ref)
+    assert err <= TOL, err
+    _check_bound(y32, y_ref[:, cols], a, sa, w, sw, rows, cols)
+    y16 = host_bf16_bits(outs[torch.bfloat16][0][:, :N])
+    np.testing.assert_array_equal(y16, _f32_to_bf16_bits(y32))
+
+
 def test_gemm_ragged_n_and_strided_output():
     p = need_gpu()
     M, N, K = 21, 18, 256

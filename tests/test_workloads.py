@@ -44,3 +44,18 @@ def test_sampled_drafts_follow_softmax():
     p = np.exp(wl.f32_from_bf16_bits(wl.bf16_bits_from_f32(z)).astype(np.float64))
     p /= p.sum()
     assert np.max(np.abs(freq - p)) < 0.015
+
+
+def test_fp8_code_bytes_cover_every_non_nan_pattern():
+    c = wl.fp8_code_bytes(600, 512, seed=9)
+    assert c.dtype == np.uint8 and c.shape == (600, 512)
+    vals = np.unique(c)
+    assert len(vals) == 254 and 0x7F not in vals and 0xFF not in vals
+    np.testing.assert_array_equal(c, wl.fp8_code_bytes(600, 512, seed=9))
+    assert not np.array_equal(c, wl.fp8_code_bytes(600, 512, seed=10))
+
+
+def test_uniform_scales_range_and_determinism():
+    s = wl.uniform_scales(1000, seed=4)
+    assert s.dtype == np.float32 and np.all(s >= 1e-3) and np.all(s < 2e-3)
+    np.testing.assert_array_equal(s, wl.uniform_scales(1000, seed=4))

@@ -11,6 +11,8 @@ from .gen import (  # noqa: F401
     f32_from_bf16_bits,
     linear_activations,
     linear_weights,
+    fp8_code_bytes,
+    uniform_scales,
     student_t_activations,
     gated_ffn_input,
     accept_logits,

@@ -64,6 +64,19 @@ def linear_weights(N: int, K: int, seed: int, std: float = 0.02) -> np.ndarray:
     return bf16_bits_from_f32(w)
 
 
+def fp8_code_bytes(rows: int, cols: int, seed: int) -> np.ndarray:
+    """Random E4M3 code bytes [rows, cols] (uint8): every byte pattern except
+    the two NaN patterns 0x7F and 0xFF, equally likely.  Operands for GEMM
+    tests that span the whole format without a quantizer in between."""
+    c = _rng(seed).integers(0, 254, size=(rows, cols), dtype=np.uint16)
+    return (c + (c >= 0x7F)).astype(np.uint8)          # 0..126 -> 0x00..0x7E, 127..253 -> 0x80..0xFE
+
+
+def uniform_scales(n: int, seed: int, lo: float = 1e-3, hi: float = 2e-3) -> np.ndarray:
+    """n fp32 scales drawn uniformly from [lo, hi)."""
+    return _rng(seed).uniform(lo, hi, size=n).astype(np.float32)
+
+
 def student_t_activations(M: int, K: int, seed: int, df: float = 3.0) -> np.ndarray:
     """Heavy-tailed activations ~ Student-t(df) [M,K] as bf16 bits."""
     x = _rng(seed).standard_t(df, size=(M, K)).astype(np.float32)
