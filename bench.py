@@ -514,8 +514,8 @@ def other_configs(torch, p, wl, reps=12):
     C2: the same four linears at M = 80 (B = 16, k = 4), HBM-bound (the
     weights dominate: 218 MB per layer); weights rotated over enough copies to
     exceed the Infinity Cache.  C5: the long-prompt FFN GEMMs at M = 4096
-    (4096 -> 14336 and 14336 -> 4096), MFMA-bound, beside hipBLASLt on the
-    same codes.  Per-token activation and per-channel weight scales, bf16 out,
+    (4096 -> 14336 and 14336 -> 4096), beside hipBLASLt on the same codes,
+    weights rotated the same way.  Per-token activation and per-channel weight scales, bf16 out,
     timed as HIP-graph replays."""
     f8 = torch.float8_e4m3fn
     g = torch.Generator(device="cuda")
@@ -569,17 +569,18 @@ def other_configs(torch, p, wl, reps=12):
     c5res = {}
     for name, K, N in (("up", c5["K1"], c5["N1"]), ("down", c5["K2"], c5["N2"])):
         a, sa = p.quantize(torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16))
-        wq = [p.quantize(torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)) for _ in range(3)]
+        ncp = max(2, int(np.ceil(300e6 / (N * K))))      # weight copies past the Infinity Cache: cold weights
+        wq = [p.quantize(torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)) for _ in range(ncp)]
         out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
         ws = torch.zeros((max(16, p.gemm_workspace_bytes(M, N, K)),), dtype=torch.uint8, device="cuda")
         fl = 2.0 * M * N * K
-        us = timed(lambda r: p.gemm(a, sa, *wq[r % 3], out=out, workspace=ws), 3)
+        us = timed(lambda r: p.gemm(a, sa, *wq[r % ncp], out=out, workspace=ws), ncp)
         c5res[name + "_us"] = round(us, 1)
         c5res[name + "_tflops"] = round(fl / (us * 1e-6) / 1e12, 1)
         c5res[name + "_pct_mfma_peak"] = round(100 * fl / (us * 1e-6) / 1e12 / PEAK_FP8_TFLOPS, 1)
         try:
-            vus = timed(lambda r: torch._scaled_mm(a.view(f8), wq[r % 3][0].view(f8).t(), scale_a=sa.view(-1, 1),
-                                                   scale_b=wq[r % 3][1].view(1, -1), out_dtype=torch.bfloat16), 3)
+            vus = timed(lambda r: torch._scaled_mm(a.view(f8), wq[r % ncp][0].view(f8).t(), scale_a=sa.view(-1, 1),
+                                                   scale_b=wq[r % ncp][1].view(1, -1), out_dtype=torch.bfloat16), ncp)
             c5res[name + "_hipblaslt_us"] = round(vus, 1)
         except Exception as e:      # a library without this FP8 path
             log(f"hipBLASLt C5 {name}: {str(e)[:100]}")
@@ -872,19 +873,27 @@ def profile_traffic(torch, p, wl):
     return 0
 
 
-def profile_gemm_c5(torch, p, wl):
-    """Kernels for counter passes on the long-prompt GEMM: three launches of
-    the C5 up projection (M = 4096, 4096 -> 14336) on different weight copies."""
+def profile_gemm_c5(torch, p, wl, rounds=5, copies=3):
+    """Kernels for kernel-trace and counter runs of the long-prompt GEMMs:
+    `rounds` rounds of the C5 up (M = 4096, 4096 -> 14336) and down
+    (14336 -> 4096) projections over `copies` weight copies each (6 x 58.7 MB
+    exceed the 256 MB Infinity Cache, so every launch finds its weights cold).
+    The two shapes run kernels of their own (256x224 and 256x256 tiles)."""
     c5 = wl.CONFIGS["C5"]
-    M, K, N = c5["M"], c5["K1"], c5["N1"]
-    a = torch.randint(0, 120, (M, K), dtype=torch.uint8, device="cuda")
+    M = c5["M"]
+    shapes = {"up": (c5["N1"], c5["K1"]), "down": (c5["K1"], c5["N1"])}
+    a = {n: torch.randint(0, 120, (M, K), dtype=torch.uint8, device="cuda") for n, (N, K) in shapes.items()}
     sa = torch.rand(M, device="cuda") * 0.01 + 1e-3
-    ws = [torch.randint(0, 120, (N, K), dtype=torch.uint8, device="cuda") for _ in range(3)]
-    sw = torch.rand(N, device="cuda") * 0.01 + 1e-3
-    out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    wsb = torch.zeros((max(p.gemm_workspace_bytes(M, N, K), 16),), dtype=torch.uint8, device="cuda")
-    for i in range(3):
-        p.gemm(a, sa, ws[i], sw, out=out, workspace=wsb)
+    ws = {n: [torch.randint(0, 120, (N, K), dtype=torch.uint8, device="cuda") for _ in range(copies)]
+          for n, (N, K) in shapes.items()}
+    sw = {n: torch.rand(N, device="cuda") * 0.01 + 1e-3 for n, (N, K) in shapes.items()}
+    out = {n: torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for n, (N, K) in shapes.items()}
+    wsb = torch.zeros((max(16, max(p.gemm_workspace_bytes(M, N, K) for N, K in shapes.values())),),
+                      dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    for r in range(rounds):
+        for n in ("up", "down"):
+            p.gemm(a[n], sa, ws[n][r % copies], sw[n], out=out[n], workspace=wsb)
     torch.cuda.synchronize()
     log("profile kernels done")
     return 0
@@ -955,8 +964,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile", choices=["traffic", "gemm_c5", "gemm_c3", "accept_c4", "step"], default=None,
                     help="for profiler runs: 'traffic' = a plain copy of 256 MiB (the counters' "
-                         "calibration), then 3 launches of the gate|up GEMM; 'gemm_c5' = 3 launches of the "
-                         "M=4096 4096->14336 GEMM; 'gemm_c3' = the four M=320 verify-step GEMMs, 10 rounds over "
+                         "calibration), then 3 launches of the gate|up GEMM; 'gemm_c5' = the M=4096 up and down "
+                         "projections, 5 rounds over 3 rotated weight copies; 'gemm_c3' = the four M=320 verify-step GEMMs, 10 rounds over "
                          "3 rotated weight copies; 'accept_c4' = 20 stochastic and 20 greedy acceptances of the "
                          "C4 logits over 3 rotated copies; 'step' = --warmup and then --steps eager verify "
                          "steps over the rotated copies, nothing else; then exit")

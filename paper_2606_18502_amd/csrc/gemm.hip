@@ -849,6 +849,52 @@ __device__ __forceinline__ void roll_step(const GemmArgs& g, int it, int nk, int
     }
 }
 
+// Epilogue of the long-prompt tiles (plain output, bf16 or fp32, never
+// split): W block by W block, each block's 4 weight scales per lane loaded
+// just before use, so that few registers besides the accumulators are live.
+// The arithmetic is store_blocks': y = fl32(fl32(acc * sa) * sw), then RNE to
+// bf16.
+template <int WTM, int WTN, bool EDGE, bool F32>
+__device__ __forceinline__ void roll_store(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
+                                           int m0, int n0, int wm, int wn, int lane) {
+    const int kg = lane >> 4;
+    const int r16 = lane & 15;
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) {
+        const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
+        float sw[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sw[r] = g.w_per_tensor ? g.sw[0] : g.sw[min(n + r, g.N - 1)];
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) {
+            const int m = m0 + (wm * WTM + j) * 16 + r16;
+            if (EDGE && m >= g.M) continue;
+            float y[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) y[r] = (acc[i][j][r] * sa_reg[j]) * sw[r];
+            if constexpr (F32) {
+                float* row = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy;
+                if (!EDGE || n + 3 < g.N) *reinterpret_cast<float4*>(row + n) = make_float4(y[0], y[1], y[2], y[3]);
+                else
+                    for (int r = 0; r < 4 && n + r < g.N; ++r) row[n + r] = y[r];
+            } else {
+                uint16_t* row = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy;
+                uint32_t bits[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) bits[r] = f32_to_bf16_rne(y[r]);
+                if (!EDGE || n + 3 < g.N) {
+                    uint2 o;
+                    o.x = bits[0] | (bits[1] << 16);
+                    o.y = bits[2] | (bits[3] << 16);
+                    *reinterpret_cast<uint2*>(row + n) = o;
+                } else {
+                    for (int r = 0; r < 4 && n + r < g.N; ++r) row[n + r] = (uint16_t)bits[r];
+                }
+            }
+        }
+    }
+}
+
 template <int WTM, int WTN>
 __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
     using R = RollCfg<WTM, WTN>;
@@ -948,9 +994,17 @@ __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
     wait_vmcnt<0>();
 
     float sa_reg[WTM];
-    float sw_reg[WTN][4];
-    load_scales<WTM, WTN>(g, sa_reg, sw_reg, m0, n0, wm, wn, lane);
-    store_tile<WTM, WTN, 2, 0>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, 0, nt, R::BM, R::BN);
+#pragma unroll
+    for (int j = 0; j < WTM; ++j)
+        sa_reg[j] = g.a_per_tensor ? g.sa[0] : g.sa[min(m0 + (wm * WTM + j) * 16 + r16, g.M - 1)];
+    const bool edge = m0 + R::BM > g.M || n0 + R::BN > g.N;
+    if (g.out_f32) {
+        if (edge) roll_store<WTM, WTN, true, true>(g, acc, sa_reg, m0, n0, wm, wn, lane);
+        else roll_store<WTM, WTN, false, true>(g, acc, sa_reg, m0, n0, wm, wn, lane);
+    } else {
+        if (edge) roll_store<WTM, WTN, true, false>(g, acc, sa_reg, m0, n0, wm, wn, lane);
+        else roll_store<WTM, WTN, false, false>(g, acc, sa_reg, m0, n0, wm, wn, lane);
+    }
 }
 
 // ---- tile configurations (plan.hpp, kTiles) ----------------------------------
