@@ -895,11 +895,77 @@ __device__ __forceinline__ void roll_store(const GemmArgs& g, const v4f (&acc)[W
     }
 }
 
+// bf16 epilogue of an interior long-prompt tile through LDS: each wave puts
+// its 128 x 16 WTN bf16 block into LDS, then writes it out row by row with
+// 16-byte stores, so every row segment leaves the CU as whole cache lines at
+// once.  (Written from the MFMA layout directly, a row's line is filled 32
+// bytes at a time across the whole epilogue and can be evicted, and written
+// back, several times while the other workgroups of the XCD stream their
+// operands.)  LDS rows of 224 bytes get a 16-byte pad; rows of 256 bytes
+// (the staging then fills both stages exactly) swap their 16-byte chunks by
+// row instead; either way the 8-byte writes of a wave and the 16-byte reads
+// hit distinct banks.  The caller has passed a workgroup barrier after the
+// K loop, so no stage is still read.
+template <int WTM, int WTN>
+__device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
+                                               int m0, int n0, int wm, int wn, int wave, int lane, char* lds) {
+    constexpr int kRowBytes = 32 * WTN;                   // 16 WTN bf16 columns
+    constexpr bool kSwap = kRowBytes == 256;
+    constexpr int kPitch = kSwap ? 256 : kRowBytes + 16;
+    constexpr int kRows = 16 * WTM;                       // 128
+    static_assert(4 * kRows * kPitch <= 2 * RollCfg<WTM, WTN>::kStageBytes, "staging fits the two stages");
+    auto at = [](int row, int byte) {
+        return (uint32_t)(row * kPitch + (kSwap ? ((((byte >> 4) ^ (row & 15)) << 4) | (byte & 15)) : byte));
+    };
+    const int kg = lane >> 4;
+    const int r16 = lane & 15;
+    const uint32_t base = lds_addr(lds) + (uint32_t)(wave * kRows * kPitch);
+#pragma unroll
+    for (int i = 0; i < WTN; ++i) {
+        const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
+        float sw[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sw[r] = g.w_per_tensor ? g.sw[0] : g.sw[n + r];
+#pragma unroll
+        for (int j = 0; j < WTM; ++j) {
+            uint32_t bits[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) bits[r] = f32_to_bf16_rne((acc[i][j][r] * sa_reg[j]) * sw[r]);
+            const uint32_t a = base + at(j * 16 + r16, i * 32 + kg * 8);
+            const uint32_t lo = bits[0] | (bits[1] << 16), hi = bits[2] | (bits[3] << 16);
+            asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"((uint64_t)lo | ((uint64_t)hi << 32)) : "memory");
+        }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // this wave's block is in LDS (only it reads it back)
+    constexpr int kChunks = kRowBytes / 16;                // 16-byte chunks per row
+    const int64_t row0 = m0 + wm * kRows;
+    const int col0 = n0 + wn * WTN * 16;
+    constexpr int kPerLane = kRows * kChunks / 64;         // 28 or 32 chunks per lane, 4 at a time
+    static_assert(kPerLane % 4 == 0, "chunks per lane");
+#pragma unroll 1
+    for (int k0 = 0; k0 < kPerLane; k0 += 4) {
+        u32x4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int c = (k0 + u) * 64 + lane;
+            asm volatile("ds_read_b128 %0, %1" : "=v"(v[u]) : "v"(base + at(c / kChunks, (c % kChunks) * 16)));
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int c = (k0 + u) * 64 + lane;
+            uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (row0 + c / kChunks) * g.ldy + col0 + (c % kChunks) * 8;
+            *reinterpret_cast<u32x4*>(dst) = v[u];
+        }
+    }
+}
+
 template <int WTM, int WTN>
 __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
     using R = RollCfg<WTM, WTN>;
-    __shared__ __attribute__((aligned(1024))) char lds0[R::kStageBytes];
-    __shared__ __attribute__((aligned(1024))) char lds1[R::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) char lds[2 * R::kStageBytes];   // two stages; the epilogue's staging
+    char* const lds0 = lds;
+    char* const lds1 = lds + R::kStageBytes;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1002,8 +1068,12 @@ __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
         if (edge) roll_store<WTM, WTN, true, true>(g, acc, sa_reg, m0, n0, wm, wn, lane);
         else roll_store<WTM, WTN, false, true>(g, acc, sa_reg, m0, n0, wm, wn, lane);
     } else {
-        if (edge) roll_store<WTM, WTN, true, false>(g, acc, sa_reg, m0, n0, wm, wn, lane);
-        else roll_store<WTM, WTN, false, false>(g, acc, sa_reg, m0, n0, wm, wn, lane);
+        if (edge) {
+            roll_store<WTM, WTN, true, false>(g, acc, sa_reg, m0, n0, wm, wn, lane);
+        } else {
+            __builtin_amdgcn_s_barrier();     // every wave is done reading the stages
+            roll_store_lds<WTM, WTN>(g, acc, sa_reg, m0, n0, wm, wn, wave, lane, lds);
+        }
     }
 }
 
