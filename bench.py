@@ -718,21 +718,34 @@ def calibration_study(torch, p, wl):
                         f"{c['public_outlier_scale']:g}), in-domain-like and mixed (half each) sets"}
 
 
-def greedy_accept_part(torch, p, step, logits, reps=10, per_graph=10):
+def greedy_accept_part(torch, p, step, logits, reps=10):
     """Greedy acceptance (temperature 0, drafts matched against the target
-    argmax) over the same C4 target logits, as HIP-graph replays; returns the
-    mean us per call and GB/s over the target logits read once."""
-    zt, zd, x, _ = logits[0]
+    argmax) over the C4 target logits, as HIP-graph replays rotating over
+    enough copies of them (4 x 82 MB) that every call reads its logits cold;
+    returns the mean us per call and GB/s over the target logits read once."""
+    cases = []
+    for zt, zd, _, _ in logits:
+        xg = torch.argmax(zd.float(), dim=-1).to(torch.int32)   # argmax drafts from the draft logits
+        cases.append((zt, xg))
+    ncp = max(len(cases), int(np.ceil(300e6 / (2.0 * cases[0][0].numel()))))
+    while len(cases) < ncp:
+        zt, xg = cases[len(cases) % len(logits)]
+        cases.append((zt.clone(), xg))
+    per_graph = ncp
     out = torch.empty_like(step.out)
     num = torch.empty_like(step.num)
-    xg = torch.argmax(zd.float(), dim=-1).to(torch.int32)       # argmax drafts from the draft logits
-    call = lambda: p.verify_accept(zt, None, xg, None, 0.0, workspace=step.aws, out_tokens=out, num_accepted=num)
-    call()
+    zt = cases[0][0]
+
+    def call(i):
+        p.verify_accept(cases[i][0], None, cases[i][1], None, 0.0, workspace=step.aws, out_tokens=out,
+                        num_accepted=num)
+
+    call(0)
     torch.cuda.synchronize()
     gr = torch.cuda.CUDAGraph()
     with torch.cuda.graph(gr):
-        for _ in range(per_graph):
-            call()
+        for i in range(per_graph):
+            call(i)
     gr.replay()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -929,8 +942,9 @@ def profile_gemm_c3(torch, p, wl, rounds=10, copies=3):
 def profile_accept_c4(torch, p, wl, reps=20, copies=3):
     """Kernels for a kernel-trace run of the acceptance alone: `reps` stochastic
     (T = 0.7) and `reps` greedy acceptances of the C4 logits, back to back,
-    rotating over `copies` copies of the logits (3 x 147.75 MB exceed the
-    256 MB Infinity Cache, so every launch reads them cold)."""
+    rotating over `copies` copies of the logits (3 x 147.75 MB) and, for
+    greedy, over copies + 2 copies of the target logits (5 x 82 MB): more than
+    the 256 MB Infinity Cache, so every launch reads them cold."""
     c = wl.CONFIGS["C4"]
     B, k, V, T = c["B"], c["k"], c["V"], c["temperature"]
     zt, zd = wl.accept_logits(B, k, V, c["seed"], wl.C4_CORRELATION, scale=c["logit_std"], rank=c["rank"])
@@ -942,14 +956,14 @@ def profile_accept_c4(torch, p, wl, reps=20, copies=3):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to("cuda")
 
     dzt, dzd = dev(zt), dev(zd)
-    zts = [dzt] + [dzt.clone() for _ in range(copies - 1)]
+    zts = [dzt] + [dzt.clone() for _ in range(copies + 1)]   # greedy reads target logits only: 5 x 82 MB
     zds = [dzd] + [dzd.clone() for _ in range(copies - 1)]
     dx, dxg, du = (torch.from_numpy(a).to("cuda") for a in (x, xg, u))
     ws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device="cuda")
     for r in range(reps):
         p.verify_accept(zts[r % copies], zds[r % copies], dx, du, T, workspace=ws)
     for r in range(reps):
-        p.verify_accept(zts[r % copies], None, dxg, None, 0.0, workspace=ws)
+        p.verify_accept(zts[r % len(zts)], None, dxg, None, 0.0, workspace=ws)
     torch.cuda.synchronize()
     log("profile kernels done")
     return 0
