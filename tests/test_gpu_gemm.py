@@ -144,6 +144,29 @@ def test_long_prompt_tiles(M, N, K, out_f32, per_tensor, strided):
     np.testing.assert_array_equal(y16, _f32_to_bf16_bits(y32))
 
 
+def test_long_prompt_operands_past_4gib():
+    """A long-prompt shape whose activation rows lie more than 4 GiB apart in
+    total ((M - 1) * lda > 2^32): the 256-wide tiles address their operands
+    with 32-bit offsets, so the launcher must take the 160x224 kernel instead.
+    Sampled rows against the oracle."""
+    p = need_gpu()
+    M, N, K = 2048, 14336, 256
+    lda = 2_100_000                                   # (M - 1) * lda > 2^32
+    say(f"long-prompt gemm with lda={lda} (A spans {(M - 1) * lda + K} bytes)")
+    a = wl.fp8_code_bytes(M, K, seed=11)
+    w = wl.fp8_code_bytes(N, K, seed=12)
+    sa, sw = wl.uniform_scales(M, seed=13), wl.uniform_scales(N, seed=14)
+    big = torch.empty(((M - 1) * lda + K,), dtype=torch.uint8, device="cuda")
+    da = big.as_strided((M, K), (lda, 1))
+    da.copy_(dev_u8(a))
+    y = host(p.gemm(da, dev_f32(sa), dev_u8(w), dev_f32(sw), out_dtype=torch.float32))
+    rows, cols = _sample(M, 48, 5), _sample(N, 48, 6)
+    y_ref = og.gemm_rows(a, sa, w, sw, rows)
+    assert og.rel_error(y[rows], y_ref) <= TOL
+    _check_bound(y, y_ref[:, cols], a, sa, w, sw, rows, cols)
+    del big
+
+
 def test_gemm_ragged_n_and_strided_output():
     p = need_gpu()
     M, N, K = 21, 18, 256
