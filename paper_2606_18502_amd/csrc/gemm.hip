@@ -912,7 +912,7 @@ __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&ac
     constexpr int kRowBytes = 32 * WTN;                   // 16 WTN bf16 columns
     constexpr bool kSwap = kRowBytes == 256;
     constexpr int kPitch = kSwap ? 256 : kRowBytes + 16;
-    constexpr int kRows = 16 * WTM;                       // 128
+    constexpr int kRows = 16 * WTM;                       // rows per wave
     static_assert(4 * kRows * kPitch <= 2 * RollCfg<WTM, WTN>::kStageBytes, "staging fits the two stages");
     auto at = [](int row, int byte) {
         return (uint32_t)(row * kPitch + (kSwap ? ((((byte >> 4) ^ (row & 15)) << 4) | (byte & 15)) : byte));
@@ -940,10 +940,11 @@ __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&ac
     constexpr int kChunks = kRowBytes / 16;                // 16-byte chunks per row
     const int64_t row0 = m0 + wm * kRows;
     const int col0 = n0 + wn * WTN * 16;
-    constexpr int kPerLane = kRows * kChunks / 64;         // 28 or 32 chunks per lane, 4 at a time
-    static_assert(kPerLane % 4 == 0, "chunks per lane");
+    constexpr int kPerLane = kRows * kChunks / 64;         // chunks per lane, 4 at a time
+    static_assert(kRows * kChunks % 64 == 0, "chunks per lane");
+    constexpr int kFull = kPerLane / 4 * 4;
 #pragma unroll 1
-    for (int k0 = 0; k0 < kPerLane; k0 += 4) {
+    for (int k0 = 0; k0 < kFull; k0 += 4) {
         u32x4 v[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -957,6 +958,15 @@ __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&ac
             uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (row0 + c / kChunks) * g.ldy + col0 + (c % kChunks) * 8;
             *reinterpret_cast<u32x4*>(dst) = v[u];
         }
+    }
+#pragma unroll
+    for (int k = kFull; k < kPerLane; ++k) {
+        const int c = k * 64 + lane;
+        u32x4 v;
+        asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(base + at(c / kChunks, (c % kChunks) * 16)));
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (row0 + c / kChunks) * g.ldy + col0 + (c % kChunks) * 8;
+        *reinterpret_cast<u32x4*>(dst) = v;
     }
 }
 
@@ -1167,9 +1177,10 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
         case 8: e = launch_cfg<8>(g, stream); break;
         case 9: e = launch_roll<9>(g, stream); break;
         case 10: e = launch_roll<10>(g, stream); break;
+        case 11: e = launch_roll<11>(g, stream); break;
         default: return hipErrorInvalidValue;
     }
-    static_assert(kTileKinds == 11, "every tile kind has a case");
+    static_assert(kTileKinds == 12, "every tile kind has a case");
     if (e != hipSuccess || p.splits == 1 || p.reduce != kReduceKernel) return e;
     const int64_t work = M * ((N + 3) / 4);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, stream, g);

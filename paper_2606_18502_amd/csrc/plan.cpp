@@ -11,6 +11,14 @@ namespace {
 
 inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
+// A CU's operand rows per K-step over the whole GEMM: the rounds of tiles the
+// 256 CUs run, times a tile's rows (BM + BN).  A CU streams its operand bytes
+// at a rate no tile shape changes, so this orders tile shapes by time.
+int64_t rows_per_cu(int64_t M, int64_t N, int kind) {
+    const int64_t tiles = ((M + tile_bm(kind) - 1) / tile_bm(kind)) * ((N + tile_bn(kind) - 1) / tile_bn(kind));
+    return ((tiles + 255) / 256) * (int64_t)(tile_bm(kind) + tile_bn(kind));
+}
+
 }  // namespace
 
 GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int reduce, int epilogue) {
@@ -84,9 +92,28 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     }
     if (M <= 320) {
         // wide N: one 160x224 tile per CU (gate|up), or 160x192 for an LM
-        // head (160x224 with a ragged last tile where N % 192 != 0)
-        if (N % 224 == 0 && N >= 224 * 64) return plan_gemm_as(M, N, K, 2, 1, kReduceNone, epilogue);
-        if (N >= 192 * 64) return plan_gemm_as(M, N, K, (N % 192 == 0) ? 4 : 2, 1, kReduceNone, epilogue);
+        // head (160x224 with a ragged last tile where N % 192 != 0); where the
+        // tiles take several rounds of the CUs (an LM head), the 160x384
+        // in-place-refill tile streams fewer operand rows per CU
+        if (N % 224 == 0 && N >= 224 * 64 && rows_per_cu(M, N, 2) <= rows_per_cu(M, N, 11))
+            return plan_gemm_as(M, N, K, 2, 1, kReduceNone, epilogue);
+        if (N >= 192 * 64) {
+            // the statistics epilogue runs on 160x192 (160x224 where it
+            // divides N better); the plain one takes the fewest rows per CU
+            const int stats_kind = (N % 192 == 0) ? 4 : 2;
+            int plain_kind = stats_kind;
+            if (rows_per_cu(M, N, 2) < rows_per_cu(M, N, plain_kind)) plain_kind = 2;
+            if (ksteps >= 2 && ksteps % 2 == 0 && rows_per_cu(M, N, 11) < rows_per_cu(M, N, plain_kind))
+                plain_kind = 11;
+            GemmPlan p = plan_gemm_as(M, N, K, epilogue == kEpiPlain ? plain_kind : stats_kind, 1, kReduceNone,
+                                      epilogue);
+            // Where the plain GEMM takes another tile than the statistics
+            // epilogue (an LM head), both walk K in order, so that the logits
+            // stored with their statistics are the plain GEMM's bit for bit
+            // (a staggered K start gained nothing measurable here).
+            if (plain_kind != stats_kind) p.krot_on = 0;
+            return p;
+        }
         // Short N (QKV, O, down).  A CU streams its operand rows at a rate
         // that no tile shape or wave count tried raised (~35 GB/s per CU at
         // every shape of the verify step), so a CU's time follows the operand
@@ -105,12 +132,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     // the fewest rows per CU (an even number of K-steps is required by them).
     int best = 2;
     if (M >= 1024 && epilogue == kEpiPlain && ksteps >= 2 && ksteps % 2 == 0) {
-        auto cost = [&](int kind) {
-            const int64_t tiles = ((M + tile_bm(kind) - 1) / tile_bm(kind)) * ((N + tile_bn(kind) - 1) / tile_bn(kind));
-            return ((tiles + 255) / 256) * (int64_t)(tile_bm(kind) + tile_bn(kind));
-        };
         for (int kind : {9, 10})
-            if (cost(kind) < cost(best)) best = kind;
+            if (rows_per_cu(M, N, kind) < rows_per_cu(M, N, best)) best = kind;
     }
     return plan_gemm_as(M, N, K, best, 1, kReduceNone, epilogue);
 }

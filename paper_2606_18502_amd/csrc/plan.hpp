@@ -28,10 +28,11 @@ struct TileShape {
 //  8    64 x 128  2x2 (32x64)           4        96 KiB  M <= 64 wide N; M <= 320 short N
 //  9   256 x 224  2x2 (128x112), roll   2       120 KiB  large M
 // 10   256 x 256  2x2 (128x128), roll   2       128 KiB  large M
+// 11   160 x 384  2x2 (80x192), roll    2       136 KiB  M <= 320, very wide N (LM head)
 constexpr TileShape kTiles[] = {
     {2, 2, 2, 2, 4, 0}, {5, 4, 1, 2, 4, 0}, {5, 7, 2, 2, 3, 0}, {8, 4, 2, 2, 3, 0}, {5, 6, 2, 2, 3, 0},
     {5, 4, 2, 2, 4, 0}, {5, 4, 4, 1, 3, 0}, {5, 2, 2, 2, 4, 0}, {2, 4, 2, 2, 4, 0}, {8, 7, 2, 2, 2, 1},
-    {8, 8, 2, 2, 2, 1},
+    {8, 8, 2, 2, 2, 1}, {5, 12, 2, 2, 2, 1},
 };
 constexpr int kTileKinds = sizeof(kTiles) / sizeof(kTiles[0]);
 constexpr int tile_bm(int k) { return 16 * kTiles[k].wtm * kTiles[k].wm; }

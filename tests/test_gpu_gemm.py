@@ -111,6 +111,7 @@ def test_gemm_parity(M, N, K):
     (4000, 4000, 1024, True, False, True),    # 256x256, ragged M and N, strided operands and output
     (2048, 7168, 512, False, False, False),   # 256x224, bf16 output
     (2000, 7000, 512, True, True, True),      # 256x224, ragged, per-tensor activation scale, strided
+    (300, 128256, 256, True, False, True),    # 160x384 (an LM head's N at M <= 320), ragged M, strided
 ])
 def test_long_prompt_tiles(M, N, K, out_f32, per_tensor, strided):
     """Random code bytes over the whole E4M3 range; sampled rows against the
