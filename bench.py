@@ -912,6 +912,33 @@ def profile_gemm_c5(torch, p, wl, rounds=5, copies=3):
     return 0
 
 
+def profile_quantize_c5(torch, p, wl, rounds=4):
+    """Kernels for kernel-trace and counter runs of the long-prompt per-token
+    quantize: `rounds` rounds of X [4096, 4096] and of the FFN intermediate
+    [4096, 14336] (bf16 in, E4M3 codes and fp32 scales out), each rotating
+    over input copies past the 256 MB Infinity Cache, then the same with a
+    static per-tensor scale.  The two shapes run different kernel instances."""
+    c5 = wl.CONFIGS["C5"]
+    M = c5["M"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(56)
+    for K in (c5["K1"], c5["K2"]):
+        ncp = max(2, int(np.ceil(300e6 / (2.0 * M * K))))
+        xs = [torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16) for _ in range(ncp)]
+        q = torch.empty((M, K), dtype=torch.uint8, device="cuda")
+        sc = torch.empty((M,), dtype=torch.float32, device="cuda")
+        s1 = torch.ones(1, dtype=torch.float32, device="cuda")
+        torch.cuda.synchronize()
+        for r in range(rounds * ncp):
+            p.quantize(xs[r % ncp], out=q, scales=sc)
+        for r in range(rounds * ncp):
+            p.quantize(xs[r % ncp], per_tensor_scale=s1, out=q)
+        torch.cuda.synchronize()
+        del xs
+    log("profile kernels done")
+    return 0
+
+
 def profile_gemm_c3(torch, p, wl, rounds=10, copies=3):
     """Kernels for kernel-trace and counter runs of the verify step's four
     GEMMs at M = 320 (QKV, O, gate|up, down) in the step's launch
@@ -976,12 +1003,14 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--copies", type=int, default=3, help="rotated copies of weights and logits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "gemm_c3", "accept_c4", "step"], default=None,
+    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "gemm_c3", "accept_c4", "step", "quantize_c5"],
+                    default=None,
                     help="for profiler runs: 'traffic' = a plain copy of 256 MiB (the counters' "
                          "calibration), then 3 launches of the gate|up GEMM; 'gemm_c5' = the M=4096 up and down "
                          "projections, 5 rounds over 3 rotated weight copies; 'gemm_c3' = the four M=320 verify-step GEMMs, 10 rounds over "
                          "3 rotated weight copies; 'accept_c4' = 20 stochastic and 20 greedy acceptances of the "
-                         "C4 logits over 3 rotated copies; 'step' = --warmup and then --steps eager verify "
+                         "C4 logits over 3 rotated copies; 'quantize_c5' = the M=4096 per-token and static quantize of "
+                         "X [4096,4096] and H [4096,14336], cold; 'step' = --warmup and then --steps eager verify "
                          "steps over the rotated copies, nothing else; then exit")
     ap.add_argument("--part", choices=["gemm", "accept", "quantize"], default=None,
                     help="time one part of the step only (cold, as in the full run) and print its figures "
@@ -1014,6 +1043,8 @@ def main(argv=None):
         return profile_accept_c4(torch, p, wl)
     if args.profile == "gemm_c3":
         return profile_gemm_c3(torch, p, wl)
+    if args.profile == "quantize_c5":
+        return profile_quantize_c5(torch, p, wl)
     acts, weights, logits = build_inputs(torch, p, wl, args.copies)
     step = Step(torch, p, wl, acts)
     if args.profile == "step":
