@@ -24,15 +24,14 @@
 //
 // K is split across workgroups (split-K) when there are fewer output tiles
 // than compute units.  The fp32 partial tiles are then added in split order
-// (deterministic), either by the last workgroup of each tile to finish (a
-// ticket per tile; it then applies the epilogue) or, for many splits of small
-// tiles, by a second kernel.
+// (deterministic) by the last workgroup of each tile to finish (a ticket per
+// tile), which then applies the epilogue.
 // Workgroup ids are remapped so that the tiles and K-splits that share
 // operands run on the same XCD (blocks are dealt round-robin to the 8 XCDs),
 // which keeps re-read operand bytes in that XCD's L2.
 //
 // Epilogue variants (a template argument, so each is its own kernel):
-//  0  the scaled output, bf16 or fp32, or the split-K partials;
+//  0  the scaled output, bf16 or fp32 (after the split-K reduction);
 //  1  bf16 logits plus per-row softmax statistics of the stored values over
 //     each wave's columns (the LM head of the verify pass);
 //  2  bf16 logits plus per-row (max, lowest column) over each wave's columns;
@@ -63,12 +62,10 @@ struct GemmArgs {
     const float* sa;
     const float* sw;
     void* y;
-    float* partial;   // kReduceKernel: [splits][M][ldp]
-    uint64_t* part;   // kReduceLast: per tile and split, the threads' accumulators (two 8-byte halves each)
-    unsigned int* tickets;   // kReduceLast: one per tile, zero between calls
-    int reduce;       // GemmReduce of the plan
+    uint64_t* part;   // split K: per tile and split, the threads' accumulators (two 8-byte halves each)
+    unsigned int* tickets;   // split K: one per tile, zero between calls
     float2* stats;    // [M][ld_stats] column-group statistics of the bf16 output (stats_mode != 0)
-    int64_t lda, ldw, ldy, ldp, ld_stats;
+    int64_t lda, ldw, ldy, ld_stats;
     int M, N, K;
     int a_per_tensor, w_per_tensor, out_f32;
     int m_tiles, n_tiles, splits, ksteps;
@@ -334,25 +331,9 @@ __device__ __forceinline__ void online_merge(float& m, float& s, float om, float
 template <int WTM, int WTN, int STATS, bool EDGE>
 __device__ __forceinline__ void store_blocks(const GemmArgs& g, const v4f (&acc)[WTN][WTM],
                                              const float (&sa_reg)[WTM], const float (&sw_reg)[WTN][4], int m0,
-                                             int n0, int wm, int wn, int lane, int split, float (&sm)[WTM],
-                                             float (&ss)[WTM]) {
+                                             int n0, int wm, int wn, int lane, float (&sm)[WTM], float (&ss)[WTM]) {
     const int kg = lane >> 4;
     const int r16 = lane & 15;
-    if (STATS == 0 && g.splits > 1 && g.reduce == kReduceKernel) {
-#pragma unroll
-        for (int j = 0; j < WTM; ++j) {
-            const int m = m0 + (wm * WTM + j) * 16 + r16;
-            float* row = g.partial + ((int64_t)split * g.M + m) * g.ldp;
-#pragma unroll
-            for (int i = 0; i < WTN; ++i) {
-                const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
-                if (EDGE && !(n < g.N && m < g.M)) continue;
-                const v4f a = acc[i][j];
-                *reinterpret_cast<float4*>(row + n) = make_float4(a[0], a[1], a[2], a[3]);
-            }
-        }
-        return;
-    }
     if (STATS == 0 && g.out_f32) {
 #pragma unroll
         for (int j = 0; j < WTM; ++j) {
@@ -436,9 +417,8 @@ __device__ __forceinline__ void store_blocks(const GemmArgs& g, const v4f (&acc)
 }
 
 // Epilogue: lane holds D[n = 4*(lane/16) + r][m = lane%16] of each 16x16
-// block; the scales were fetched into registers before the main loop.  With a
-// K split the fp32 partial goes to the workspace instead.  Tiles wholly
-// inside the output take the unchecked path.
+// block; the scales were fetched into registers before the main loop.  Tiles
+// wholly inside the output take the unchecked path.
 //
 // STATS 3 (SiLU-gated output, no K split): the tile's weight rows pair gate
 // and up rows (w_row), and each lane pair kg, kg ^ 2 of a block exchanges its
@@ -456,7 +436,7 @@ __device__ __forceinline__ void store_blocks(const GemmArgs& g, const v4f (&acc)
 template <int WTM, int WTN, int WN, int STATS>
 __device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
                                            const float (&sw_reg)[WTN][4], int m0, int n0, int wm, int wn, int lane,
-                                           int split, int nt, int BM, int BN) {
+                                           int nt, int BM, int BN) {
     float sm[WTM], ss[WTM];      // STATS 1: running max and sum; STATS 2: best value and (int bits) its column
 #pragma unroll
     for (int j = 0; j < WTM; ++j) {
@@ -464,9 +444,9 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[W
         ss[j] = STATS == 2 ? __int_as_float(0x7fffffff) : 0.0f;
     }
     if (m0 + BM <= g.M && n0 + BN <= g.N)
-        store_blocks<WTM, WTN, STATS, false>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, sm, ss);
+        store_blocks<WTM, WTN, STATS, false>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, sm, ss);
     else
-        store_blocks<WTM, WTN, STATS, true>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, sm, ss);
+        store_blocks<WTM, WTN, STATS, true>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, sm, ss);
     if constexpr (STATS == 1 || STATS == 2) {
         const int kg = lane >> 4;
         const int r16 = lane & 15;
@@ -495,7 +475,7 @@ __device__ __forceinline__ uint64_t pack2(float lo, float hi) {
     return ((uint64_t)__float_as_uint(hi) << 32) | (uint64_t)__float_as_uint(lo);
 }
 
-// Split-K reduced in the kernel (kReduceLast).  Every workgroup of a split
+// Split-K reduced in the kernel.  Every workgroup of a split
 // tile stores its fp32 partial tile with device-coherent stores (relaxed
 // agent-scope atomics: written through the non-coherent caches, so a
 // workgroup on any XCD reads them), waits until all of them are
@@ -672,52 +652,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
     wait_vmcnt<0>();   // no direct-to-LDS write may outlive the workgroup
 
     if constexpr (STATS == 0 && REDUCE_LAST) {
-        if (g.splits > 1 && g.reduce == kReduceLast) {
+        if (g.splits > 1) {
             __shared__ int s_last;
             if (!reduce_last<WTM, WTN, C::kThreads>(g, acc, tile, split, tid, &s_last)) return;
         }
     }
-    store_tile<WTM, WTN, WN, STATS>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, split, nt, C::BM, C::BN);
-}
-
-// Sum the split-K partials in split order, then scale and convert.
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g) {
-    const int64_t quads = (int64_t)((g.N + 3) / 4);
-    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (int64_t)g.M * quads) return;
-    const int m = (int)(idx / quads);
-    const int n = (int)(idx % quads) * 4;
-    float4 s = *reinterpret_cast<const float4*>(g.partial + (int64_t)m * g.ldp + n);
-    for (int z = 1; z < g.splits; ++z) {
-        const float4 p = *reinterpret_cast<const float4*>(g.partial + ((int64_t)z * g.M + m) * g.ldp + n);
-        s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
-    }
-    const float a[4] = {s.x, s.y, s.z, s.w};
-    const float sa = g.a_per_tensor ? g.sa[0] : g.sa[m];
-    float y[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const float sw = g.w_per_tensor ? g.sw[0] : g.sw[n + r < g.N ? n + r : g.N - 1];
-        y[r] = (a[r] * sa) * sw;
-    }
-    if (g.out_f32) {
-        float* dst = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy + n;
-        if (n + 3 < g.N) {
-            *reinterpret_cast<float4*>(dst) = make_float4(y[0], y[1], y[2], y[3]);
-        } else {
-            for (int r = 0; r < 4 && n + r < g.N; ++r) dst[r] = y[r];
-        }
-    } else {
-        uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy + n;
-        if (n + 3 < g.N) {
-            uint2 o;
-            o.x = f32_to_bf16_rne(y[0]) | (f32_to_bf16_rne(y[1]) << 16);
-            o.y = f32_to_bf16_rne(y[2]) | (f32_to_bf16_rne(y[3]) << 16);
-            *reinterpret_cast<uint2*>(dst) = o;
-        } else {
-            for (int r = 0; r < 4 && n + r < g.N; ++r) dst[r] = (uint16_t)f32_to_bf16_rne(y[r]);
-        }
-    }
+    store_tile<WTM, WTN, WN, STATS>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, nt, C::BM, C::BN);
 }
 
 // ---- long prompts: 256-wide tiles, operand fragments refilled in place ------
@@ -1117,7 +1057,7 @@ hipError_t launch_cfg(GemmArgs g, hipStream_t stream) {
         }
     }
     if (g.stats_mode != 0) return hipErrorInvalidValue;
-    if (!REDUCE_LAST && g.splits > 1 && g.reduce == kReduceLast) return hipErrorInvalidValue;
+    if (!REDUCE_LAST && g.splits > 1) return hipErrorInvalidValue;
     hipLaunchKernelGGL((gemm_fp8_kernel<WTM, WTN, WM, WN, STAGES, 0, REDUCE_LAST>), dim3(total), dim3(C::kThreads), 0,
                        stream, g);
     return hipGetLastError();
@@ -1145,7 +1085,7 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
     if (kTiles[p.kind].roll && ((uint64_t)(M - 1) * (uint64_t)lda + kBK > (1ull << 32) ||
                                 (uint64_t)(N - 1) * (uint64_t)ldw + kBK > (1ull << 32))) {
         // its per-lane offsets are 32-bit: operands past 4 GiB take the 160x224 kernel
-        const GemmPlan q = plan_gemm_as(M, N, K, 2, 1, kReduceNone, kEpiPlain);
+        const GemmPlan q = plan_gemm_as(M, N, K, 2, 1, kEpiPlain);
         return launch_gemm(q, a, lda, sa, a_per_tensor, w, ldw, sw, w_per_tensor, M, N, K, y, ldy, out_f32,
                            workspace, stream, stats_mode, c2, stats, ld_stats, silu_inter);
     }
@@ -1155,10 +1095,8 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
     g.a = a; g.w = w; g.sa = sa; g.sw = sw; g.y = y;
     char* ws = reinterpret_cast<char*>(workspace);
     g.tickets = reinterpret_cast<unsigned int*>(ws);
-    g.partial = reinterpret_cast<float*>(ws ? ws + p.part_off : nullptr);
     g.part = reinterpret_cast<uint64_t*>(ws ? ws + p.part_off : nullptr);
-    g.reduce = p.reduce;
-    g.lda = lda; g.ldw = ldw; g.ldy = ldy; g.ldp = p.ldp;
+    g.lda = lda; g.ldw = ldw; g.ldy = ldy;
     g.M = (int)M; g.N = (int)N; g.K = (int)K;
     g.a_per_tensor = a_per_tensor; g.w_per_tensor = w_per_tensor; g.out_f32 = out_f32;
     g.m_tiles = p.m_tiles; g.n_tiles = p.n_tiles; g.splits = p.splits; g.ksteps = (int)(K / kBK);
@@ -1181,10 +1119,7 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
         default: return hipErrorInvalidValue;
     }
     static_assert(kTileKinds == 12, "every tile kind has a case");
-    if (e != hipSuccess || p.splits == 1 || p.reduce != kReduceKernel) return e;
-    const int64_t work = M * ((N + 3) / 4);
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, stream, g);
-    return hipGetLastError();
+    return e;
 }
 
 }  // namespace specfp8

@@ -30,11 +30,10 @@ struct GemmPlan {
     int kind;              // tile configuration (plan.hpp, kTiles)
     int m_tiles, n_tiles;  // output tiles
     int splits;            // K-splits (1 = none)
-    int reduce;            // how split partials are added (plan.hpp, GemmReduce)
+    int reduce;            // kReduceLast when K is split (plan.hpp, GemmReduce)
     int group_m;           // > 1: tile order in groups of group_m M-tiles
     int krot_on;           // staggered K start per N-tile
     int64_t stat_groups;   // column groups per row of the epilogue statistics (n_tiles * waves across N)
-    int64_t ldp;           // row stride of the fp32 partial tiles (kReduceKernel)
     size_t part_off;       // byte offset of the partial tiles in the workspace (tickets before it)
     size_t workspace_bytes;
 };
@@ -42,10 +41,9 @@ struct GemmPlan {
 // SiLU-gated output; the last two keep one workgroup per output tile.
 enum GemmEpilogue { kEpiPlain = 0, kEpiStats = 1, kEpiSilu = 2 };
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue = kEpiPlain);
-// The plan for an explicit tile kind, K split and reduction (plan_gemm's
-// choices are made through it; also used to compare configurations).
-GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int reduce,
-                      int epilogue = kEpiPlain);
+// The plan for an explicit tile kind and K split (plan_gemm's choices are
+// made through it; also used to compare configurations).
+GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int epilogue = kEpiPlain);
 // stats_mode 0: plain GEMM; 1/2: also the per-(row, column group) statistics
 // of the bf16 output (softmax in base 2 with c2 = log2(e)/T, or argmax) into
 // stats [M][ld_stats]; requires p.splits == 1.

@@ -21,7 +21,7 @@ int64_t rows_per_cu(int64_t M, int64_t N, int kind) {
 
 }  // namespace
 
-GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int reduce, int epilogue) {
+GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int epilogue) {
     GemmPlan p{};
     if (kind < 0 || kind >= kTileKinds) kind = 2;
     // the statistics epilogues never split K; the 160x224 tile has no
@@ -35,20 +35,17 @@ GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int
     const int bm = tile_bm(kind), bn = tile_bn(kind);
     p.m_tiles = (int)((M + bm - 1) / bm);
     p.n_tiles = (int)((N + bn - 1) / bn);
+    const int64_t tiles = (int64_t)p.m_tiles * p.n_tiles;
+    // the 160x224 kernel has no in-kernel reduction (its registers are
+    // full), and a tile without a ticket cannot be reduced: no K split
+    if (kind == 2 || tiles > (int64_t)(kGemmTicketBytes / sizeof(unsigned int))) splits = 1;
     const int ksteps = (int)(K / kGemmBK);
     if (splits > ksteps) splits = ksteps;
     if (splits < 1) splits = 1;
     // every split must own at least one K-step after ceil division
     while (splits > 1 && (int64_t)((ksteps + splits - 1) / splits) * (splits - 1) >= ksteps) --splits;
     p.splits = splits;
-    const int64_t tiles = (int64_t)p.m_tiles * p.n_tiles;
-    if (splits == 1) reduce = kReduceNone;
-    else if (reduce != kReduceKernel && reduce != kReduceLast) reduce = kReduceLast;
-    // the 160x224 kernel has no in-kernel reduction (its registers are full);
-    // more tiles than tickets fall back to the reduction kernel as well
-    if (reduce == kReduceLast && (kind == 2 || tiles > (int64_t)(kGemmTicketBytes / sizeof(unsigned int))))
-        reduce = kReduceKernel;
-    p.reduce = reduce;
+    p.reduce = splits > 1 ? kReduceLast : kReduceNone;
     // Many M-tiles (long prompts): tiles in groups of 4 M-tiles with K walked
     // in step, so the 32 tiles an XCD runs at once re-read 4 activation and
     // 8 weight tiles from its L2 (5-8% at M = 4096).  Few M-tiles keep the
@@ -60,14 +57,9 @@ GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int
         p.krot_on = 0;
     }
     p.stat_groups = (int64_t)p.n_tiles * kTiles[kind].wn;
-    p.ldp = (N + 3) / 4 * 4;
     p.part_off = kGemmTicketBytes;
-    if (reduce == kReduceKernel)
-        p.workspace_bytes = p.part_off + align256((size_t)splits * (size_t)M * (size_t)p.ldp * sizeof(float));
-    else if (reduce == kReduceLast)
-        p.workspace_bytes = p.part_off + align256((size_t)tiles * splits * (size_t)bm * bn * sizeof(float));
-    else
-        p.workspace_bytes = 0;
+    p.workspace_bytes =
+        splits > 1 ? p.part_off + align256((size_t)tiles * splits * (size_t)bm * bn * sizeof(float)) : 0;
     return p;
 }
 
@@ -80,15 +72,16 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
         // per workgroup.  Very wide N (gate|up) fills the chip unsplit;
         // otherwise 64x64 tiles with K split until about 256 workgroups run
         // or every split holds at most 32 K-steps, keeping >= 8 K-steps per
-        // split.
-        if (N >= 192 * 64) return plan_gemm_as(M, N, K, M <= 64 ? 8 : 1, 1, kReduceNone, epilogue);
+        // split.  The last workgroup of a tile adds its partial tiles: one
+        // launch fewer, 1-2 us per GEMM at these sizes.
+        if (N >= 192 * 64) return plan_gemm_as(M, N, K, M <= 64 ? 8 : 1, 1, epilogue);
         const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);
         splits = (int)(256 / tiles);
         if (splits < (ksteps + 31) / 32) splits = (ksteps + 31) / 32;
         const int max_split = ksteps / 8 > 0 ? ksteps / 8 : 1;
         if (splits > max_split) splits = max_split;
         if (splits > 16) splits = 16;
-        return plan_gemm_as(M, N, K, 0, splits, kReduceKernel, epilogue);
+        return plan_gemm_as(M, N, K, 0, splits, epilogue);
     }
     if (M <= 320) {
         // wide N: one 160x224 tile per CU (gate|up), or 160x192 for an LM
@@ -96,7 +89,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
         // tiles take several rounds of the CUs (an LM head), the 160x384
         // in-place-refill tile streams fewer operand rows per CU
         if (N % 224 == 0 && N >= 224 * 64 && rows_per_cu(M, N, 2) <= rows_per_cu(M, N, 11))
-            return plan_gemm_as(M, N, K, 2, 1, kReduceNone, epilogue);
+            return plan_gemm_as(M, N, K, 2, 1, epilogue);
         if (N >= 192 * 64) {
             // the statistics epilogue runs on 160x192 (160x224 where it
             // divides N better); the plain one takes the fewest rows per CU
@@ -105,8 +98,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
             if (rows_per_cu(M, N, 2) < rows_per_cu(M, N, plain_kind)) plain_kind = 2;
             if (ksteps >= 2 && ksteps % 2 == 0 && rows_per_cu(M, N, 11) < rows_per_cu(M, N, plain_kind))
                 plain_kind = 11;
-            GemmPlan p = plan_gemm_as(M, N, K, epilogue == kEpiPlain ? plain_kind : stats_kind, 1, kReduceNone,
-                                      epilogue);
+            GemmPlan p = plan_gemm_as(M, N, K, epilogue == kEpiPlain ? plain_kind : stats_kind, 1, epilogue);
             // Where the plain GEMM takes another tile than the statistics
             // epilogue (an LM head), both walk K in order, so that the logits
             // stored with their statistics are the plain GEMM's bit for bit
@@ -122,9 +114,9 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
         // (cold weights) chose: long K (down, 14336 -> 4096) 80x128 tiles with
         // K split in 2; N <= 4096 (O) 160x64 split in 2; else (QKV) 64x128
         // unsplit.
-        if (K >= 2 * N) return plan_gemm_as(M, N, K, 1, 2, kReduceLast, epilogue);
-        if (N <= 4096) return plan_gemm_as(M, N, K, 7, 2, kReduceLast, epilogue);
-        return plan_gemm_as(M, N, K, 8, 1, kReduceNone, epilogue);
+        if (K >= 2 * N) return plan_gemm_as(M, N, K, 1, 2, epilogue);
+        if (N <= 4096) return plan_gemm_as(M, N, K, 7, 2, epilogue);
+        return plan_gemm_as(M, N, K, 8, 1, epilogue);
     }
     // Long prompts.  A CU's time is its operand bytes: per tile (BM + BN)
     // rows per K-step, times the rounds of tiles every CU runs.  The 256-wide
@@ -135,7 +127,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
         for (int kind : {9, 10})
             if (rows_per_cu(M, N, kind) < rows_per_cu(M, N, best)) best = kind;
     }
-    return plan_gemm_as(M, N, K, best, 1, kReduceNone, epilogue);
+    return plan_gemm_as(M, N, K, best, 1, epilogue);
 }
 
 AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {

@@ -41,14 +41,14 @@ constexpr int tile_threads(int k) { return 64 * kTiles[k].wm * kTiles[k].wn; }
 
 constexpr int kGemmBK = 128;   // bytes (= E4M3 elements) of K per step
 
-// Split-K reductions.  kReduceKernel: fp32 partial tiles [splits][M][ldp] go
-// to the workspace and a second kernel adds them in split order.
-// kReduceLast: every workgroup of a split tile stores its partial tile, and
-// the last of them to arrive (an atomic ticket per tile) adds all of them in
-// split order and writes the output.  The tickets live in the first
-// kGemmTicketBytes of the workspace, which must be zero before the first call
-// and which every call leaves zero again.
-enum GemmReduce { kReduceNone = 0, kReduceKernel = 1, kReduceLast = 2 };
+// Split-K reduction: every workgroup of a split tile stores its partial tile
+// in the workspace, and the last of them to arrive (an atomic ticket per
+// tile) adds all of them in split order and writes the output.  The tickets
+// live in the first kGemmTicketBytes of the workspace, which must be zero
+// before the first call and which every call leaves zero again.  Plans with
+// more tiles than tickets, and the 160x224 tile (no registers left for the
+// reduction), do not split K.
+enum GemmReduce { kReduceNone = 0, kReduceLast = 1 };
 constexpr size_t kGemmTicketBytes = 16384;   // 4096 tile tickets
 
 // ---- acceptance ---------------------------------------------------------------
