@@ -238,9 +238,11 @@ __global__ __launch_bounds__(kAThreads) void greedy_partial_kernel(AcceptArgs a)
 }
 
 __global__ __launch_bounds__(1024) void greedy_final_kernel(AcceptArgs a) {
-    __shared__ int g[17];
+    __shared__ int g[17], s_x[16];
     const int b = blockIdx.x;
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    // the drafts are loaded first, so their round trip overlaps the merge
+    const int32_t xt = t < a.k ? a.x[(int64_t)b * a.k + t] : 0;
     // wave wv merges positions wv, wv+16, ... (one round for k < 16); lanes
     // stride over the slices
     const int nw = (int)(blockDim.x >> 6);
@@ -272,12 +274,13 @@ __global__ __launch_bounds__(1024) void greedy_final_kernel(AcceptArgs a) {
         }
         if (lane == 0) g[pos] = bi;
     }
+    if (t < a.k) s_x[t] = xt;
     __syncthreads();
     if (t <= a.k) {
         // a_b = number of leading drafts equal to the target argmax
         int acc = a.k;
         for (int i = 0; i < a.k; ++i)
-            if (a.x[(int64_t)b * a.k + i] != g[i]) { acc = i; break; }
+            if (s_x[i] != g[i]) { acc = i; break; }
         int32_t* out = a.out + (int64_t)b * (a.k + 1);
         out[t] = t < acc ? g[t] : (t == acc ? g[acc] : -1);
         if (t == 0) a.num[b] = acc;
@@ -526,8 +529,9 @@ template <bool VEC>
 __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     __shared__ float sM[33], sZ[33];
     __shared__ double s_rm[kAThreads];
-    __shared__ int s_acc[16];
+    __shared__ int s_acc[16], s_x[16];
     __shared__ int s_j, s_last;
+    __shared__ float s_uk;
     __shared__ double sh[kWavesPerBlock];
     __shared__ int s_own, s_lastpos;
     __shared__ double s_base;
@@ -538,12 +542,13 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     const int k = a.k;
 
     // The operands of the accept tests are loaded first (draft id, then the
-    // two logits at it), so their round trips overlap the statistics merge.
+    // two logits at it), so their round trips overlap the statistics merge;
+    // so are the resampling uniform and the drafts the outputs repeat.
     int32_t xi = -1;
     float zx_t = 0.0f, zx_d = 0.0f, ui = 0.0f;
+    if (t <= k) ui = a.u[(int64_t)b * (k + 1) + t];
     if (t < k) {
         xi = a.x[(int64_t)b * k + t];
-        ui = a.u[(int64_t)b * (k + 1) + t];
         if (xi >= 0 && xi < a.V) {
             zx_t = bf16_to_f32(a.zt[((int64_t)b * (k + 1) + t) * a.V + xi]);
             if (a.zd) zx_d = bf16_to_f32(a.zd[((int64_t)b * k + t) * a.V + xi]);
@@ -589,6 +594,8 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
             if (lane == 0) { sM[r] = M; sZ[r] = Z; }
         }
     }
+    if (t < k) s_x[t] = xi;
+    if (t == k) s_uk = ui;
     __syncthreads();
 
     // 2. accept tests of the k drafts, evaluated in parallel (identical in
@@ -628,7 +635,7 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
             d.md = sM[k + 1 + j];
             d.inv_zd = 1.0f / sZ[k + 1 + j];
         } else {
-            d.skip = a.x[(int64_t)b * k + j];
+            d.skip = s_x[j];
         }
     }
 
@@ -689,7 +696,7 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
         v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
         block_scan_d(v1, sh, lo1, hi1, R);
     }
-    const double target = (double)a.u[(int64_t)b * (k + 1) + k] * R;
+    const double target = (double)s_uk * R;
     find_owner(v1, lo1, hi1, 0.0, target, &s_own, &s_base, &s_lastpos);
     const int64_t cs = s_own;
     const double base2 = s_base;
@@ -723,7 +730,7 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
         else pick = 0;
         if (lane <= k) {
             int32_t* out = a.out + (int64_t)b * (k + 1);
-            out[lane] = lane < j ? a.x[(int64_t)b * k + lane] : (lane == j ? (int)min(e0 + pick, a.V - 1) : -1);
+            out[lane] = lane < j ? s_x[lane] : (lane == j ? (int)min(e0 + pick, a.V - 1) : -1);
             if (lane == 0) {
                 a.num[b] = j;
                 a.ctr[b] = 0u;
@@ -743,13 +750,23 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
 
 constexpr int kMaxTree = 64;   // nodes per sequence
 
-// Merged (max logit, lowest index) of row r of sequence b, for lanes of one wave.
-__device__ __forceinline__ int merged_argmax(const AcceptArgs& a, int b, int r, int lane) {
+// Entry `lane` of row r's (max logit, lowest index) statistics, or the
+// neutral (-inf, INT_MAX) past the row's entries.
+__device__ __forceinline__ float2 argmax_entry(const AcceptArgs& a, int b, int r, int lane) {
     uint32_t nst;
     const float2* st = row_stats(a, b, r, nst);
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-    for (int64_t c0 = lane; c0 < nst; c0 += 8 * 64) {
+    return (uint32_t)lane < nst ? st[lane] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
+}
+
+// Merged (max logit, lowest index) of row r of sequence b, for lanes of one
+// wave; `first` is the row's entry `lane` (argmax_entry), loaded beforehand.
+// The order of `better` is total, so the merge order does not matter.
+__device__ __forceinline__ int merged_argmax(const AcceptArgs& a, int b, int r, int lane, float2 first) {
+    uint32_t nst;
+    const float2* st = row_stats(a, b, r, nst);
+    float bv = first.x;
+    int bi = __float_as_int(first.y);
+    for (int64_t c0 = lane + 64; c0 < nst; c0 += 8 * 64) {
         float2 pv[8];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
@@ -792,16 +809,33 @@ __global__ __launch_bounds__(1024) void tree_greedy_kernel(AcceptArgs a) {
     const int b = blockIdx.x;
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const int N = a.k;
+    // the tree and the first statistics entry of every row of the wave are
+    // loaded before anything waits for them (one round trip for all); the
+    // tree reaches shared memory after the merge
+    int par = -2, xv = -1;
     if (t < N) {
-        s_par[t] = a.parent[(int64_t)b * N + t];
-        s_x[t] = a.x[(int64_t)b * N + t];
+        par = a.parent[(int64_t)b * N + t];
+        xv = a.x[(int64_t)b * N + t];
     }
-    // rows over all waves (16): each merge is one dependent round trip, so
-    // the N+1 <= 65 rows take at most 5 in a row
-    const int nw = (int)(blockDim.x >> 6);
-    for (int r = wv; r <= N; r += nw) {
-        const int bi = merged_argmax(a, b, r, lane);
+    // rows over the 16 waves: wave wv merges rows wv, wv+16, ...
+    constexpr int kGreedyWaves = 1024 / kWave;
+    constexpr int kRowsPerWaveG = (kMaxTree + 1 + kGreedyWaves - 1) / kGreedyWaves;
+    float2 first[kRowsPerWaveG];
+#pragma unroll
+    for (int i = 0; i < kRowsPerWaveG; ++i) {
+        const int r = wv + i * kGreedyWaves;
+        first[i] = r <= N ? argmax_entry(a, b, r, lane) : make_float2(-INFINITY, __int_as_float(0x7fffffff));
+    }
+#pragma unroll
+    for (int i = 0; i < kRowsPerWaveG; ++i) {
+        const int r = wv + i * kGreedyWaves;
+        if (r > N) break;
+        const int bi = merged_argmax(a, b, r, lane, first[i]);
         if (lane == 0) g[r] = bi;
+    }
+    if (t < N) {
+        s_par[t] = par;
+        s_x[t] = xv;
     }
     __syncthreads();
     if (t == 0) {
@@ -849,20 +883,17 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
     const int lane = t & 63, wv = t >> 6;
     const int N = a.k;
 
-    // the tree, the uniforms and the candidates' logits are loaded first, so
-    // their round trips overlap the statistics merge
+    // the tree, the uniforms, the first statistics entries and the
+    // candidates' logits are loaded before anything waits for them, so their
+    // round trips overlap (the logits' addresses need the tree); they reach
+    // shared memory after the merge
     int par = -2, xv = -1;
-    float zx = 0.0f;
-    bool ok = false;
+    float uv = 0.0f;
     if (t < N) {
         par = a.parent[(int64_t)b * N + t];
         xv = a.x[(int64_t)b * N + t];
-        s_par[t] = par;
-        s_x[t] = xv;
-        ok = par >= -1 && par < t && xv >= 0 && xv < a.V;
-        if (ok) zx = bf16_to_f32(a.zt[((int64_t)b * (N + 1) + par + 1) * a.V + xv]);
     }
-    if (t <= N) s_u[t] = a.u[(int64_t)b * (N + 1) + t];
+    if (t <= N) uv = a.u[(int64_t)b * (N + 1) + t];
     // wave wv merges rows wv, wv+4, ...: the first entry of every one of its
     // rows is loaded before any is merged (one round trip for all of them),
     // then each lane merges its entries in index order
@@ -877,6 +908,12 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
             const float2* st = row_stats(a, b, r, nst);
             if ((uint32_t)lane < nst) first[i] = st[lane];
         }
+    }
+    float zx = 0.0f;
+    bool ok = false;
+    if (t < N) {
+        ok = par >= -1 && par < t && xv >= 0 && xv < a.V;
+        if (ok) zx = bf16_to_f32(a.zt[((int64_t)b * (N + 1) + par + 1) * a.V + xv]);
     }
 #pragma unroll
     for (int i = 0; i < kTreeRowsPerWave; ++i) {
@@ -900,6 +937,11 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
         const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));
         if (lane == 0) { sM[r] = M; sZ[r] = Z; }
     }
+    if (t < N) {
+        s_par[t] = par;
+        s_x[t] = xv;
+    }
+    if (t <= N) s_u[t] = uv;
     __syncthreads();
     // every candidate's probability under its parent's row; t - M is formed
     // exactly in double (bf16 * fp32 fits in 53 bits), as for chains
