@@ -72,6 +72,7 @@ struct AcceptArgs {
     const float2* tst;     // target rows' statistics from the LM-head epilogue, or null
     int64_t ldtst;         // row stride of tst (entries)
     uint32_t ntst;         // entries per target row in tst
+    float2* tsm;           // [B][k+1] tst merged to one entry per row by the statistics kernel, or null
     double* chunkm;        // [B][nchunk] residual mass per chunk
     double* finem;         // [B][nchunk][256] residual mass per 64-element range
     unsigned int* ctr;     // [B]
@@ -88,6 +89,10 @@ struct AcceptArgs {
 // the LM-head epilogue when given, else (and for draft rows) the streamed ones.
 __device__ __forceinline__ const float2* row_stats(const AcceptArgs& a, int b, int r, uint32_t& n) {
     if ((uint32_t)r < a.rt0) {
+        if (a.tsm) {
+            n = 1;
+            return a.tsm + (int64_t)b * (a.k + 1) + r;
+        }
         n = a.ntst;
         return a.tst + ((int64_t)b * (a.k + 1) + r) * a.ldtst;
     }
@@ -251,17 +256,18 @@ __global__ __launch_bounds__(1024) void greedy_final_kernel(AcceptArgs a) {
         const float2* st = row_stats(a, b, pos, nst);
         float bv = -INFINITY;
         int bi = 0x7fffffff;
-        // loads issued 8 per lane before they are compared (a row may hold
-        // over a thousand entries when they come from the LM-head epilogue)
-        for (int64_t c0 = lane; c0 < nst; c0 += 8 * 64) {
-            float2 pv[8];
+        // loads issued 24 per lane before they are compared: a row may hold
+        // over a thousand entries when they come from the LM-head epilogue
+        // (1336 for V = 128256), which then take one round trip
+        for (int64_t c0 = lane; c0 < nst; c0 += 24 * 64) {
+            float2 pv[24];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
+            for (int q = 0; q < 24; ++q) {
                 const int64_t c = c0 + q * 64;
                 pv[q] = c < nst ? st[c] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
             }
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
+            for (int q = 0; q < 24; ++q) {
                 const int pi = __float_as_int(pv[q].y);
                 if (better(pv[q].x, pi, bv, bi)) { bv = pv[q].x; bi = pi; }
             }
@@ -312,9 +318,59 @@ __device__ __forceinline__ float2 slice_stats(const uint16_t* z, const Raw& raw,
     return make_float2(M, wave_sum(s));
 }
 
+// Online merge of (max, sum 2^(t - max)) pairs.
+__device__ __forceinline__ void merge_ms(float& m, float& z, float om, float oz) {
+    if (om == -INFINITY) return;
+    if (om > m) {
+        z = (m == -INFINITY ? 0.0f : z * exp2f(m - om)) + oz;
+        m = om;
+    } else {
+        z += oz * exp2f(om - m);
+    }
+}
+
+// (M, Z) of the n statistics entries st[0..n) merged over one wave: lane l
+// merges entries l, l + 64, l + 128, ... in that order (`first` is its entry
+// l, loaded by the caller, or (-inf, 0) past n), then the wave combines the
+// lanes.  A row given as its single merged entry gives back that entry
+// exactly (the other lanes add zeros).
+__device__ __forceinline__ float2 merge_row_ms(const float2* st, uint32_t n, int lane, float2 first) {
+    float m = -INFINITY, z = 0.0f;
+    merge_ms(m, z, first.x, first.y);
+    // loads issued 8 per lane before they are merged, in entry order
+    for (int64_t q0 = lane + kWave; q0 < n; q0 += 8 * kWave) {
+        float2 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int64_t q = q0 + u * kWave;
+            v[u] = q < n ? st[q] : make_float2(-INFINITY, 0.0f);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) merge_ms(m, z, v[u].x, v[u].y);
+    }
+    const float M = wave_max(m);
+    const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));
+    return make_float2(M, Z);
+}
+
 template <bool VEC>
 __global__ __launch_bounds__(kAThreads) void stoch_stats_kernel(AcceptArgs a) {
     const int lane = threadIdx.x & (kWave - 1);
+    if (a.tsm) {
+        // Target statistics from the LM-head epilogue (many entries per row):
+        // merged here to one entry per row, so that every sampling block
+        // reads one entry per target row.  The waves with the highest ids
+        // hold the fewest items (often none), so they take the merges.
+        const uint32_t gw = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+        const uint32_t GW = gridDim.x * kWavesPerBlock;
+        const uint32_t rows = (uint32_t)a.B * (uint32_t)(a.k + 1);
+        for (uint32_t m = GW - 1 - gw; m < rows; m += GW) {
+            const float2* st = a.tst + (int64_t)m * a.ldtst;
+            const float2 first = (uint32_t)lane < a.ntst ? st[lane] : make_float2(-INFINITY, 0.0f);
+            const float2 r = merge_row_ms(st, a.ntst, lane, first);
+            if (lane == 0) a.tsm[m] = r;
+        }
+    }
     auto row_of = [&](uint32_t row) -> const uint16_t* {
         const int64_t b = row / a.Rs;
         const int r = (int)(a.rt0 + row % a.Rs);
@@ -509,17 +565,6 @@ __device__ __forceinline__ double load_coherent(const double* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Online merge of (max, sum 2^(t - max)) pairs.
-__device__ __forceinline__ void merge_ms(float& m, float& z, float om, float oz) {
-    if (om == -INFINITY) return;
-    if (om > m) {
-        z = (m == -INFINITY ? 0.0f : z * exp2f(m - om)) + oz;
-        m = om;
-    } else {
-        z += oz * exp2f(om - m);
-    }
-}
-
 // Sampling from the residual (or bonus) distribution of position j by inverse
 // CDF in vocabulary order, in three levels: every block stores the masses of
 // its chunk's 256 ranges of 64 elements (thread t owns range t) and the chunk
@@ -576,22 +621,8 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
         if (r < (int)a.R) {
             uint32_t nst;
             const float2* st = row_stats(a, b, r, nst);
-            float m = -INFINITY, z = 0.0f;
-            merge_ms(m, z, first[i].x, first[i].y);
-            // loads issued 8 per lane before they are merged, in entry order
-            for (int64_t q0 = lane + kWave; q0 < nst; q0 += 8 * kWave) {
-                float2 v[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int64_t q = q0 + u * kWave;
-                    v[u] = q < nst ? st[q] : make_float2(-INFINITY, 0.0f);
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) merge_ms(m, z, v[u].x, v[u].y);
-            }
-            const float M = wave_max(m);
-            const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));
-            if (lane == 0) { sM[r] = M; sZ[r] = Z; }
+            const float2 mz = merge_row_ms(st, nst, lane, first[i]);
+            if (lane == 0) { sM[r] = mz.x; sZ[r] = mz.y; }
         }
     }
     if (t < k) s_x[t] = xi;
@@ -921,21 +952,8 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
         if (r > N) break;
         uint32_t nst;
         const float2* st = row_stats(a, b, r, nst);
-        float m = -INFINITY, z = 0.0f;
-        merge_ms(m, z, first[i].x, first[i].y);
-        for (int64_t q0 = lane + kWave; q0 < nst; q0 += 8 * kWave) {
-            float2 v[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const int64_t qi = q0 + q * kWave;
-                v[q] = qi < nst ? st[qi] : make_float2(-INFINITY, 0.0f);
-            }
-#pragma unroll
-            for (int q = 0; q < 8; ++q) merge_ms(m, z, v[q].x, v[q].y);
-        }
-        const float M = wave_max(m);
-        const float Z = wave_sum(m == -INFINITY ? 0.0f : z * exp2f(m - M));
-        if (lane == 0) { sM[r] = M; sZ[r] = Z; }
+        const float2 mz = merge_row_ms(st, nst, lane, first[i]);
+        if (lane == 0) { sM[r] = mz.x; sZ[r] = mz.y; }
     }
     if (t < N) {
         s_par[t] = par;
@@ -1134,7 +1152,7 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
     int cus = 0;
     if (hipError_t e = device_cus(&cus); e != hipSuccess) return e;
     AcceptArgs a{};
-    a.tst = tstats; a.ntst = (uint32_t)n_tstats; a.ldtst = ld_tstats;
+    a.tst = tstats; a.ntst = (uint32_t)n_tstats; a.ldtst = ld_tstats; a.tsm = nullptr;
     char* ws = reinterpret_cast<char*>(workspace);
     a.zt = zt; a.zd = zd; a.x = x; a.u = u; a.out = out_tokens; a.num = num_accepted;
     a.stats = reinterpret_cast<float2*>(ws + p.stats_off);
@@ -1163,6 +1181,10 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
     a.Rs = a.R - a.rt0;
     a.c2 = (float)(1.4426950408889634 / (double)temperature);
     a.items = (uint32_t)(B * a.Rs * p.nschunk);
+    // with target statistics and streamed draft rows, the statistics kernel
+    // merges the target rows' entries into the statistics area after the
+    // streamed rows' (B*Rs*nslice + B*(k+1) <= B*R*nslice entries)
+    if (tstats && a.items > 0) a.tsm = a.stats + (int64_t)B * a.Rs * p.nschunk;
     if (a.items > 0) {
         const unsigned g1 = stream_blocks(a.items, cus);
         if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
