@@ -271,6 +271,9 @@ spec_status spec_fp8_gemm_silu_mul(const uint8_t* a, int64_t lda, const float* a
  * stats   pairs of fp32 [M, ld_stats] (ld_stats counted in pairs, >= the group
  *         count), 8-byte aligned.
  * temperature finite and >= 0 (SPEC_ERR_VALUE otherwise).  No workspace.
+ * Where the plan takes the 160 x 384 tile (a wide vocabulary), a tile's rows of
+ * A and of W must each span at most 4 GiB: 159*lda + 128 <= 2^32 and
+ * 383*ldw + 128 <= 2^32 (SPEC_ERR_UNSUPPORTED otherwise).
  * spec_logit_stats_count returns 0 for arguments spec_fp8_gemm would reject.
  */
 size_t spec_logit_stats_count(int64_t M, int64_t V, int64_t K);

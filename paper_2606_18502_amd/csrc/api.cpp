@@ -105,7 +105,7 @@ spec_status spec_fp8_gemm_logit_stats(const uint8_t* a, int64_t lda, const float
     const specfp8::GemmPlan plan = specfp8::plan_gemm(M > 0 ? M : 1, V, K, specfp8::kEpiStats);
     st = specfp8::check_logit_stats(M, V, temperature, logits, ld_logits, stats, ld_stats, plan.stat_groups);
     if (st != SPEC_OK || M == 0) return st;
-    if (!grid_fits(plan)) return SPEC_ERR_UNSUPPORTED;
+    if (!grid_fits(plan) || !specfp8::gemm_strides_fit(plan.kind, lda, ldw)) return SPEC_ERR_UNSUPPORTED;
     const float c2 = temperature > 0.0f ? (float)(1.4426950408889634 / (double)temperature) : 0.0f;
     return from_hip(specfp8::launch_gemm(plan, a, lda, a_scale, a_mode == SPEC_SCALE_PER_TENSOR, w, ldw, w_scale,
                                          w_mode == SPEC_SCALE_PER_TENSOR, M, V, K, logits, ld_logits, 0, nullptr,

@@ -326,6 +326,68 @@ __device__ __forceinline__ void online_merge(float& m, float& s, float om, float
     m = M;
 }
 
+// Statistics epilogues (STATS 1: (max t, sum 2^(t - max)) of t = fl32(z *
+// c2); STATS 2: (max z, lowest column)) of the bf16 values a lane stores, per
+// row block j of its wave tile: start values, then 4 consecutive columns
+// n..n+3 at a time (a lane visits its columns in increasing order, so a
+// strict comparison keeps the lowest column of a tie; columns past the edge
+// count as absent).
+template <int WTM, int STATS>
+__device__ __forceinline__ void stats_init(float (&sm)[WTM], float (&ss)[WTM]) {
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) {
+        sm[j] = STATS == 1 ? -FLT_MAX : -INFINITY;
+        ss[j] = STATS == 2 ? __int_as_float(0x7fffffff) : 0.0f;
+    }
+}
+
+template <int STATS, bool EDGE>
+__device__ __forceinline__ void stats_add4(const GemmArgs& g, const uint32_t (&bits)[4], int n, float& sm, float& ss) {
+    if constexpr (STATS == 1) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float t = bf16_to_f32(bits[r]) * g.c2;
+            online_add(sm, ss, (!EDGE || n + r < g.N) ? t : -INFINITY);
+        }
+    } else if constexpr (STATS == 2) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float z = bf16_to_f32(bits[r]);
+            const bool gt = (!EDGE || n + r < g.N) && z > sm;
+            sm = gt ? z : sm;
+            ss = gt ? __int_as_float(n + r) : ss;
+        }
+    }
+}
+
+// The 4 lanes r16 + 16 kg that share a row combine their statistics by two
+// xor shuffles in a fixed order; lane kg = 0 stores the row's entry of
+// column group `col` (rows from mrow0 + 16 j + r16).  Empty groups store
+// (-inf, 0) (STATS 1) or (-inf, INT_MAX bits) (STATS 2).
+template <int WTM, int STATS>
+__device__ __forceinline__ void stats_store(const GemmArgs& g, const float (&sm)[WTM], const float (&ss)[WTM], int mrow0,
+                                            int lane, int64_t col) {
+    const int kg = lane >> 4;
+    const int r16 = lane & 15;
+#pragma unroll
+    for (int j = 0; j < WTM; ++j) {
+        float m1 = sm[j], s1 = ss[j];
+        if (STATS == 1 && m1 == -FLT_MAX) m1 = -INFINITY;      // no column of this group in this lane
+#pragma unroll
+        for (int o = 16; o <= 32; o <<= 1) {
+            const float m2 = __shfl_xor(m1, o, 64);
+            const float s2 = __shfl_xor(s1, o, 64);
+            if (STATS == 2) {
+                if (beats(m2, __float_as_int(s2), m1, __float_as_int(s1))) { m1 = m2; s1 = s2; }
+            } else {
+                online_merge(m1, s1, m2, s2);
+            }
+        }
+        const int m = mrow0 + j * 16 + r16;
+        if (kg == 0 && m < g.M) g.stats[(int64_t)m * g.ld_stats + col] = make_float2(m1, s1);
+    }
+}
+
 // The 16x16 blocks of one wave's tile.  EDGE: the tile crosses the last row
 // or column, so every store (and every statistic) is bounds-checked.
 template <int WTM, int WTN, int STATS, bool EDGE>
@@ -385,23 +447,7 @@ __device__ __forceinline__ void store_blocks(const GemmArgs& g, const v4f (&acc)
                 }
                 continue;
             }
-            if constexpr (STATS == 1) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float t = bf16_to_f32(bits[r]) * g.c2;
-                    online_add(sm[j], ss[j], (!EDGE || n + r < g.N) ? t : -INFINITY);
-                }
-            } else if constexpr (STATS == 2) {
-                // a lane visits its columns in increasing order, so a strict
-                // comparison keeps the lowest column of a tie
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float z = bf16_to_f32(bits[r]);
-                    const bool gt = (!EDGE || n + r < g.N) && z > sm[j];
-                    sm[j] = gt ? z : sm[j];
-                    ss[j] = gt ? __int_as_float(n + r) : ss[j];
-                }
-            }
+            stats_add4<STATS, EDGE>(g, bits, n, sm[j], ss[j]);
             if (!EDGE || n + 3 < g.N) {
                 if (!EDGE || m < g.M) {
                     uint2 o;
@@ -438,37 +484,13 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, const v4f (&acc)[W
                                            const float (&sw_reg)[WTN][4], int m0, int n0, int wm, int wn, int lane,
                                            int nt, int BM, int BN) {
     float sm[WTM], ss[WTM];      // STATS 1: running max and sum; STATS 2: best value and (int bits) its column
-#pragma unroll
-    for (int j = 0; j < WTM; ++j) {
-        sm[j] = STATS == 1 ? -FLT_MAX : -INFINITY;
-        ss[j] = STATS == 2 ? __int_as_float(0x7fffffff) : 0.0f;
-    }
+    stats_init<WTM, STATS>(sm, ss);
     if (m0 + BM <= g.M && n0 + BN <= g.N)
         store_blocks<WTM, WTN, STATS, false>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, sm, ss);
     else
         store_blocks<WTM, WTN, STATS, true>(g, acc, sa_reg, sw_reg, m0, n0, wm, wn, lane, sm, ss);
-    if constexpr (STATS == 1 || STATS == 2) {
-        const int kg = lane >> 4;
-        const int r16 = lane & 15;
-        const int64_t col = (int64_t)nt * WN + wn;
-#pragma unroll
-        for (int j = 0; j < WTM; ++j) {
-            float m1 = sm[j], s1 = ss[j];
-            if (STATS == 1 && m1 == -FLT_MAX) m1 = -INFINITY;      // no column of this group in this lane
-#pragma unroll
-            for (int o = 16; o <= 32; o <<= 1) {
-                const float m2 = __shfl_xor(m1, o, 64);
-                const float s2 = __shfl_xor(s1, o, 64);
-                if (STATS == 2) {
-                    if (beats(m2, __float_as_int(s2), m1, __float_as_int(s1))) { m1 = m2; s1 = s2; }
-                } else {
-                    online_merge(m1, s1, m2, s2);
-                }
-            }
-            const int m = m0 + (wm * WTM + j) * 16 + r16;
-            if (kg == 0 && m < g.M) g.stats[(int64_t)m * g.ld_stats + col] = make_float2(m1, s1);
-        }
-    }
+    if constexpr (STATS == 1 || STATS == 2)
+        stats_store<WTM, STATS>(g, sm, ss, m0 + wm * WTM * 16, lane, (int64_t)nt * WN + wn);
 }
 
 __device__ __forceinline__ uint64_t pack2(float lo, float hi) {
@@ -743,15 +765,15 @@ __device__ __forceinline__ void static_for(F&& f) {
 // one); NEXT: refill the fragments with step it+1 (there is one).  ab/wb: this
 // lane's A and W read bases in stage S ^ 1.
 template <class R, int WTM, int WTN, int S, bool LOADS, bool NEXT>
-__device__ __forceinline__ void roll_step(const GemmArgs& g, int it, int nk, int krot,
+__device__ __forceinline__ void roll_step(const uint8_t* a0, const uint8_t* w0, int it, int nk, int krot,
                                           const uint32_t (&off)[R::kGroupsPerWave], uint32_t lds_stage,
                                           const uint32_t (&ab)[2], const uint32_t (&wb)[2], v4f (&acc)[WTN][WTM],
                                           Frags<WTM, WTN>& f) {
     wait_vmcnt<0>();                      // step it+1 has landed (this wave's loads) ...
     __builtin_amdgcn_s_barrier();         // ... and every wave's; every wave has read step it from stage S
     const int64_t kref = (int64_t)((it + 2 + krot) % nk) * kBK;
-    const uint8_t* abase = g.a + kref;
-    const uint8_t* wbase = g.w + kref;
+    const uint8_t* abase = a0 + kref;
+    const uint8_t* wbase = w0 + kref;
     constexpr int kMfma = WTM * WTN;
     constexpr int kG = R::kGroupsPerWave;
     constexpr int kLSpan = (kMfma * kLoadSpan8 + 7) / 8;
@@ -789,14 +811,13 @@ __device__ __forceinline__ void roll_step(const GemmArgs& g, int it, int nk, int
     }
 }
 
-// Epilogue of the long-prompt tiles (plain output, bf16 or fp32, never
-// split): W block by W block, each block's 4 weight scales per lane loaded
-// just before use, so that few registers besides the accumulators are live.
-// The arithmetic is store_blocks': y = fl32(fl32(acc * sa) * sw), then RNE to
-// bf16.
-template <int WTM, int WTN, bool EDGE, bool F32>
-__device__ __forceinline__ void roll_store(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
-                                           int m0, int n0, int wm, int wn, int lane) {
+// fp32 epilogue of the in-place-refill tiles (never split): W block by W
+// block, each block's 4 weight scales per lane loaded just before use, so
+// that few registers besides the accumulators are live.  The arithmetic is
+// store_blocks': y = fl32(fl32(acc * sa) * sw).
+template <int WTM, int WTN, bool EDGE>
+__device__ __forceinline__ void roll_store_f32(const GemmArgs& g, const v4f (&acc)[WTN][WTM],
+                                               const float (&sa_reg)[WTM], int m0, int n0, int wm, int wn, int lane) {
     const int kg = lane >> 4;
     const int r16 = lane & 15;
 #pragma unroll
@@ -812,43 +833,39 @@ __device__ __forceinline__ void roll_store(const GemmArgs& g, const v4f (&acc)[W
             float y[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) y[r] = (acc[i][j][r] * sa_reg[j]) * sw[r];
-            if constexpr (F32) {
-                float* row = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy;
-                if (!EDGE || n + 3 < g.N) *reinterpret_cast<float4*>(row + n) = make_float4(y[0], y[1], y[2], y[3]);
-                else
-                    for (int r = 0; r < 4 && n + r < g.N; ++r) row[n + r] = y[r];
-            } else {
-                uint16_t* row = reinterpret_cast<uint16_t*>(g.y) + (int64_t)m * g.ldy;
-                uint32_t bits[4];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) bits[r] = f32_to_bf16_rne(y[r]);
-                if (!EDGE || n + 3 < g.N) {
-                    uint2 o;
-                    o.x = bits[0] | (bits[1] << 16);
-                    o.y = bits[2] | (bits[3] << 16);
-                    *reinterpret_cast<uint2*>(row + n) = o;
-                } else {
-                    for (int r = 0; r < 4 && n + r < g.N; ++r) row[n + r] = (uint16_t)bits[r];
-                }
-            }
+            float* row = reinterpret_cast<float*>(g.y) + (int64_t)m * g.ldy;
+            if (!EDGE || n + 3 < g.N) *reinterpret_cast<float4*>(row + n) = make_float4(y[0], y[1], y[2], y[3]);
+            else
+                for (int r = 0; r < 4 && n + r < g.N; ++r) row[n + r] = y[r];
         }
     }
 }
 
-// bf16 epilogue of an interior long-prompt tile through LDS: each wave puts
-// its 128 x 16 WTN bf16 block into LDS, then writes it out row by row with
-// 16-byte stores, so every row segment leaves the CU as whole cache lines at
-// once.  (Written from the MFMA layout directly, a row's line is filled 32
-// bytes at a time across the whole epilogue and can be evicted, and written
-// back, several times while the other workgroups of the XCD stream their
-// operands.)  LDS rows of 224 bytes get a 16-byte pad; rows of 256 bytes
+// bf16 epilogue of the in-place-refill tiles through LDS: each wave puts its
+// 16 WTM x 16 WTN bf16 block into LDS (y = fl32(fl32(acc * sa) * sw), then
+// RNE), then writes it out row by row with 16-byte stores, so every row
+// segment leaves the CU as whole cache lines at once.  (Written from the MFMA
+// layout directly, a row's line is filled 32 bytes at a time across the whole
+// epilogue and can be evicted, and written back, several times while the
+// other workgroups of the XCD stream their operands.)  LDS rows of 256 bytes
 // (the staging then fills both stages exactly) swap their 16-byte chunks by
-// row instead; either way the 8-byte writes of a wave and the 16-byte reads
-// hit distinct banks.  The caller has passed a workgroup barrier after the
-// K loop, so no stage is still read.
-template <int WTM, int WTN>
+// row; other rows get a 16-byte pad; either way the 8-byte writes of a wave
+// and the 16-byte reads hit distinct banks.  The caller has passed a
+// workgroup barrier after the K loop, so no stage is still read.  EDGE: the
+// tile crosses the last row or column: weight scales are read clamped, and
+// rows >= M and columns >= N are neither stored nor counted.
+//
+// STATS 1, 2 (the LM head): after its stores, every lane reads back from LDS
+// the 4 WTN consecutive columns kg * 4 WTN ... of row 16 j + r16 of its wave
+// block, for every row block j, and forms their statistics: STATS 1 the
+// maximum t = fl32(z * c2) first, then the sum of 2^(t - max); STATS 2 the
+// maximum z and its lowest column (columns visited in increasing order, a
+// strict comparison).  stats_store then combines the 4 lanes of a row, so
+// each wave writes the statistics of its 16 WTN columns (one column group).
+template <int WTM, int WTN, int STATS, bool EDGE>
 __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&acc)[WTN][WTM], const float (&sa_reg)[WTM],
-                                               int m0, int n0, int wm, int wn, int wave, int lane, char* lds) {
+                                               int m0, int n0, int wm, int wn, int wave, int lane, char* lds,
+                                               int64_t col_group) {
     constexpr int kRowBytes = 32 * WTN;                   // 16 WTN bf16 columns
     constexpr bool kSwap = kRowBytes == 256;
     constexpr int kPitch = kSwap ? 256 : kRowBytes + 16;
@@ -865,7 +882,7 @@ __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&ac
         const int n = n0 + (wn * WTN + i) * 16 + 4 * kg;
         float sw[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sw[r] = g.w_per_tensor ? g.sw[0] : g.sw[n + r];
+        for (int r = 0; r < 4; ++r) sw[r] = g.w_per_tensor ? g.sw[0] : g.sw[EDGE ? min(n + r, g.N - 1) : n + r];
 #pragma unroll
         for (int j = 0; j < WTM; ++j) {
             uint32_t bits[4];
@@ -880,6 +897,18 @@ __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&ac
     constexpr int kChunks = kRowBytes / 16;                // 16-byte chunks per row
     const int64_t row0 = m0 + wm * kRows;
     const int col0 = n0 + wn * WTN * 16;
+    // one 16-byte chunk of 8 columns: whole, or (EDGE) the columns below N
+    auto put = [&](int c, const u32x4& v) {
+        const int64_t m = row0 + c / kChunks;
+        const int n = col0 + (c % kChunks) * 8;
+        uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + m * g.ldy + n;
+        if (!EDGE || (m < g.M && n + 7 < g.N)) {
+            *reinterpret_cast<u32x4*>(dst) = v;
+        } else if (m < g.M) {
+            const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
+            for (int e = 0; e < 8 && n + e < g.N; ++e) dst[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+        }
+    };
     constexpr int kPerLane = kRows * kChunks / 64;         // chunks per lane, 4 at a time
     static_assert(kRows * kChunks % 64 == 0, "chunks per lane");
     constexpr int kFull = kPerLane / 4 * 4;
@@ -893,11 +922,9 @@ __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&ac
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int c = (k0 + u) * 64 + lane;
-            uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (row0 + c / kChunks) * g.ldy + col0 + (c % kChunks) * 8;
-            *reinterpret_cast<u32x4*>(dst) = v[u];
-        }
+        for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(v[u]));   // no use moves above the wait
+#pragma unroll
+        for (int u = 0; u < 4; ++u) put((k0 + u) * 64 + lane, v[u]);
     }
 #pragma unroll
     for (int k = kFull; k < kPerLane; ++k) {
@@ -905,12 +932,73 @@ __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&ac
         u32x4 v;
         asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(base + at(c / kChunks, (c % kChunks) * 16)));
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + (row0 + c / kChunks) * g.ldy + col0 + (c % kChunks) * 8;
-        *reinterpret_cast<u32x4*>(dst) = v;
+        asm volatile("" : "+v"(v));
+        put(c, v);
+    }
+    if constexpr (STATS == 1 || STATS == 2) {
+        static_assert(WTN % 2 == 0, "a lane's columns are whole 16-byte chunks");
+        constexpr int kLaneCols = 4 * WTN;
+        constexpr int kLaneChunks = kLaneCols / 8;
+        const int c0 = col0 + kg * kLaneCols;              // this lane's first column
+        float sm[WTM], ss[WTM];
+#pragma unroll 1
+        for (int j = 0; j < WTM; ++j) {
+            u32x4 v[kLaneChunks];
+#pragma unroll
+            for (int q = 0; q < kLaneChunks; ++q)
+                asm volatile("ds_read_b128 %0, %1"
+                             : "=v"(v[q])
+                             : "v"(base + at(j * 16 + r16, kg * kLaneCols * 2 + q * 16)));
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            // the values are read only now: no use may move above the wait
+#pragma unroll
+            for (int q = 0; q < kLaneChunks; ++q) asm volatile("" : "+v"(v[q]));
+            auto z_of = [&](int q, int e) {
+                return __uint_as_float(((e & 1) ? v[q][e >> 1] : v[q][e >> 1] << 16) & 0xffff0000u);
+            };
+            if constexpr (STATS == 1) {
+                float zmax = -INFINITY;
+#pragma unroll
+                for (int q = 0; q < kLaneChunks; ++q)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (!EDGE || c0 + q * 8 + e < g.N) zmax = fmaxf(zmax, z_of(q, e));
+                const float M = zmax * g.c2;                 // = max t (c2 > 0; rounding is monotone)
+                float s = 0.0f;
+                if (zmax != -INFINITY) {
+#pragma unroll
+                    for (int q = 0; q < kLaneChunks; ++q)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (!EDGE || c0 + q * 8 + e < g.N)
+                                s += __builtin_amdgcn_exp2f(z_of(q, e) * g.c2 - M);
+                }
+                sm[j] = M;
+                ss[j] = s;
+            } else {
+                float best = -INFINITY;
+                int bi = 0x7fffffff;
+#pragma unroll
+                for (int q = 0; q < kLaneChunks; ++q)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float z = z_of(q, e);
+                        const bool gt = (!EDGE || c0 + q * 8 + e < g.N) && z > best;
+                        best = gt ? z : best;
+                        bi = gt ? c0 + q * 8 + e : bi;
+                    }
+                sm[j] = best;
+                ss[j] = __int_as_float(bi);
+            }
+        }
+        stats_store<WTM, STATS>(g, sm, ss, (int)row0, lane, col_group);
     }
 }
 
-template <int WTM, int WTN>
+// STATS 1, 2: the statistics epilogue of the LM head (bf16 logits plus their
+// per-(row, wave column group) statistics, as gemm_fp8_kernel's), with the
+// same logits as STATS 0.
+template <int WTM, int WTN, int STATS>
 __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
     using R = RollCfg<WTM, WTN>;
     __shared__ __attribute__((aligned(1024))) char lds[2 * R::kStageBytes];   // two stages; the epilogue's staging
@@ -942,7 +1030,11 @@ __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
     const int nk = g.ksteps;
     const int krot = g.krot_on ? (nt * 7) % nk : 0;
 
-    // per-lane offsets of the load groups (rows past the edge re-read the last row)
+    // per-lane offsets of the load groups from the tile's first operand rows
+    // (rows past the edge re-read the last row); a tile spans less than
+    // 4 GiB of either operand (the host checks), the whole operand may not
+    const uint8_t* const a0 = g.a + (int64_t)m0 * g.lda;
+    const uint8_t* const w0 = g.w + (int64_t)n0 * g.ldw;
     uint32_t off[R::kGroupsPerWave];
 #pragma unroll
     for (int q = 0; q < R::kGroupsPerWave; ++q) {
@@ -950,10 +1042,10 @@ __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
         const int chunk = (lane & 7) ^ swz(row);
         if (q < WTM) {
             const int m = min(m0 + row, g.M - 1);
-            off[q] = (uint32_t)m * (uint32_t)g.lda + (uint32_t)(chunk * 16);
+            off[q] = (uint32_t)(m - m0) * (uint32_t)g.lda + (uint32_t)(chunk * 16);
         } else {
             const int n = min(n0 + row - R::BM, g.N - 1);
-            off[q] = (uint32_t)n * (uint32_t)g.ldw + (uint32_t)(chunk * 16);
+            off[q] = (uint32_t)(n - n0) * (uint32_t)g.ldw + (uint32_t)(chunk * 16);
         }
     }
     // LDS: the group's 1 KiB of each stage (m0 of the loads), and this lane's
@@ -983,7 +1075,7 @@ __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
         const int64_t kb = (int64_t)((min(s, nk - 1) + krot) % nk) * kBK;
 #pragma unroll
         for (int q = 0; q < R::kGroupsPerWave; ++q)
-            roll_load(q < WTM ? g.a + kb : g.w + kb, off[q], (s ? ld1 : ld0) + q * 4096);
+            roll_load(q < WTM ? a0 + kb : w0 + kb, off[q], (s ? ld1 : ld0) + q * 4096);
     }
     wait_vmcnt<R::kGroupsPerWave>();
     __builtin_amdgcn_s_barrier();
@@ -999,7 +1091,7 @@ __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
     // their stage, then the last pair (the plan takes this kernel only for an
     // even number of K-steps), so no step is behind a branch
 #define SPEC_ROLL(S, LOADS, NEXT, IT) \
-    roll_step<R, WTM, WTN, S, LOADS, NEXT>(g, IT, nk, krot, off, S ? ld1 : ld0, ab[S ^ 1], wb[S ^ 1], acc, f)
+    roll_step<R, WTM, WTN, S, LOADS, NEXT>(a0, w0, IT, nk, krot, off, S ? ld1 : ld0, ab[S ^ 1], wb[S ^ 1], acc, f)
     for (int it = 0; it + 2 < nk; it += 2) {
         SPEC_ROLL(0, true, true, it);
         SPEC_ROLL(1, true, true, it + 1);
@@ -1014,16 +1106,14 @@ __global__ __launch_bounds__(256) void gemm_fp8_roll_kernel(GemmArgs g) {
     for (int j = 0; j < WTM; ++j)
         sa_reg[j] = g.a_per_tensor ? g.sa[0] : g.sa[min(m0 + (wm * WTM + j) * 16 + r16, g.M - 1)];
     const bool edge = m0 + R::BM > g.M || n0 + R::BN > g.N;
-    if (g.out_f32) {
-        if (edge) roll_store<WTM, WTN, true, true>(g, acc, sa_reg, m0, n0, wm, wn, lane);
-        else roll_store<WTM, WTN, false, true>(g, acc, sa_reg, m0, n0, wm, wn, lane);
+    if (STATS == 0 && g.out_f32) {
+        if (edge) roll_store_f32<WTM, WTN, true>(g, acc, sa_reg, m0, n0, wm, wn, lane);
+        else roll_store_f32<WTM, WTN, false>(g, acc, sa_reg, m0, n0, wm, wn, lane);
     } else {
-        if (edge) {
-            roll_store<WTM, WTN, true, false>(g, acc, sa_reg, m0, n0, wm, wn, lane);
-        } else {
-            __builtin_amdgcn_s_barrier();     // every wave is done reading the stages
-            roll_store_lds<WTM, WTN>(g, acc, sa_reg, m0, n0, wm, wn, wave, lane, lds);
-        }
+        __builtin_amdgcn_s_barrier();     // every wave is done reading the stages
+        const int64_t col_group = (int64_t)nt * 2 + wn;
+        if (edge) roll_store_lds<WTM, WTN, STATS, true>(g, acc, sa_reg, m0, n0, wm, wn, wave, lane, lds, col_group);
+        else roll_store_lds<WTM, WTN, STATS, false>(g, acc, sa_reg, m0, n0, wm, wn, wave, lane, lds, col_group);
     }
 }
 
@@ -1069,9 +1159,20 @@ hipError_t launch_roll(const GemmArgs& g, hipStream_t stream) {
     static_assert(kTiles[KIND].roll && kTiles[KIND].wm == 2 && kTiles[KIND].wn == 2 && kTiles[KIND].stages == 2,
                   "roll tiles are 2x2 waves over 2 stages");
     static_assert(RollCfg<WTM, WTN>::BM == tile_bm(KIND) && RollCfg<WTM, WTN>::BN == tile_bn(KIND), "tile table");
-    if (g.splits != 1 || g.stats_mode != 0 || g.silu_inter != 0 || g.ksteps < 2 || g.ksteps % 2 != 0)
-        return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_fp8_roll_kernel<WTM, WTN>), dim3(g.m_tiles * g.n_tiles), dim3(256), 0, stream, g);
+    if (g.splits != 1 || g.silu_inter != 0 || g.ksteps < 2 || g.ksteps % 2 != 0) return hipErrorInvalidValue;
+    const dim3 grid(g.m_tiles * g.n_tiles);
+    if constexpr (KIND == kRollStatsKind) {
+        if (g.stats_mode == 1 && !g.out_f32) {
+            hipLaunchKernelGGL((gemm_fp8_roll_kernel<WTM, WTN, 1>), grid, dim3(256), 0, stream, g);
+            return hipGetLastError();
+        }
+        if (g.stats_mode == 2 && !g.out_f32) {
+            hipLaunchKernelGGL((gemm_fp8_roll_kernel<WTM, WTN, 2>), grid, dim3(256), 0, stream, g);
+            return hipGetLastError();
+        }
+    }
+    if (g.stats_mode != 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_fp8_roll_kernel<WTM, WTN, 0>), grid, dim3(256), 0, stream, g);
     return hipGetLastError();
 }
 
@@ -1082,9 +1183,12 @@ hipError_t launch_gemm(const GemmPlan& p, const uint8_t* a, int64_t lda, const f
                        int64_t N, int64_t K, void* y, int64_t ldy, int out_f32, void* workspace,
                        hipStream_t stream, int stats_mode, float c2, float2* stats, int64_t ld_stats,
                        int64_t silu_inter) {
-    if (kTiles[p.kind].roll && ((uint64_t)(M - 1) * (uint64_t)lda + kBK > (1ull << 32) ||
-                                (uint64_t)(N - 1) * (uint64_t)ldw + kBK > (1ull << 32))) {
-        // its per-lane offsets are 32-bit: operands past 4 GiB take the 160x224 kernel
+    if (!gemm_strides_fit(p.kind, lda, ldw)) {
+        // the in-place-refill kernels address a tile's operand rows with 32-bit
+        // offsets: strides too long for that take the 160x224 kernel, plain
+        // output only (its statistics layout would differ; the host refuses
+        // such a statistics call before it gets here)
+        if (stats_mode != 0 || silu_inter != 0) return hipErrorInvalidValue;
         const GemmPlan q = plan_gemm_as(M, N, K, 2, 1, kEpiPlain);
         return launch_gemm(q, a, lda, sa, a_per_tensor, w, ldw, sw, w_per_tensor, M, N, K, y, ldy, out_f32,
                            workspace, stream, stats_mode, c2, stats, ld_stats, silu_inter);

@@ -44,6 +44,11 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue = kEpiPlain);
 // The plan for an explicit tile kind and K split (plan_gemm's choices are
 // made through it; also used to compare configurations).
 GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int epilogue = kEpiPlain);
+// Whether the kernel of tile kind `kind` can address operands with these row
+// strides: the in-place-refill kernels need a tile's rows of A and of W to
+// span at most 4 GiB ((BM - 1) lda + 128 and (BN - 1) ldw + 128 <= 2^32);
+// the others take any stride.
+bool gemm_strides_fit(int kind, int64_t lda, int64_t ldw);
 // stats_mode 0: plain GEMM; 1/2: also the per-(row, column group) statistics
 // of the bf16 output (softmax in base 2 with c2 = log2(e)/T, or argmax) into
 // stats [M][ld_stats]; requires p.splits == 1.

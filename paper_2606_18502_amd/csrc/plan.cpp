@@ -27,8 +27,10 @@ GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int
     // the statistics epilogues never split K; the 160x224 tile has no
     // statistics variant (it would spill), 160x192 takes its place
     if (epilogue == kEpiStats && kind == 2) kind = 4;
-    // the in-place-refill kernels have the plain epilogue only and no K split
-    if (kTiles[kind].roll && epilogue != kEpiPlain) kind = epilogue == kEpiStats ? 4 : 2;
+    // the in-place-refill kernels have the plain epilogue only (kRollStatsKind
+    // also the statistics one) and no K split
+    if (kTiles[kind].roll && epilogue != kEpiPlain && !(epilogue == kEpiStats && kind == kRollStatsKind))
+        kind = epilogue == kEpiStats ? 4 : 2;
     if (kTiles[kind].roll) splits = 1;
     if (epilogue != kEpiPlain) splits = 1;
     p.kind = kind;
@@ -63,6 +65,13 @@ GemmPlan plan_gemm_as(int64_t M, int64_t N, int64_t K, int kind, int splits, int
     return p;
 }
 
+bool gemm_strides_fit(int kind, int64_t lda, int64_t ldw) {
+    if (kind < 0 || kind >= kTileKinds || !kTiles[kind].roll) return true;
+    const uint64_t lim = 1ull << 32;
+    return (uint64_t)(tile_bm(kind) - 1) * (uint64_t)lda + kGemmBK <= lim &&
+           (uint64_t)(tile_bn(kind) - 1) * (uint64_t)ldw + kGemmBK <= lim;
+}
+
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
     const int ksteps = (int)(K / kGemmBK);
     int splits = 1;
@@ -91,19 +100,22 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int epilogue) {
         if (N % 224 == 0 && N >= 224 * 64 && rows_per_cu(M, N, 2) <= rows_per_cu(M, N, 11))
             return plan_gemm_as(M, N, K, 2, 1, epilogue);
         if (N >= 192 * 64) {
-            // the statistics epilogue runs on 160x192 (160x224 where it
-            // divides N better); the plain one takes the fewest rows per CU
-            const int stats_kind = (N % 192 == 0) ? 4 : 2;
+            // the plain epilogue takes the fewest rows per CU among 160x192
+            // (160x224 where it divides N better), 160x224 and 160x384; the
+            // statistics epilogue takes the same tile where it has one
+            // (160x384), else 160x192 (160x224 where it divides N better)
+            int stats_kind = (N % 192 == 0) ? 4 : 2;
             int plain_kind = stats_kind;
             if (rows_per_cu(M, N, 2) < rows_per_cu(M, N, plain_kind)) plain_kind = 2;
             if (ksteps >= 2 && ksteps % 2 == 0 && rows_per_cu(M, N, 11) < rows_per_cu(M, N, plain_kind))
                 plain_kind = 11;
+            if (plain_kind == kRollStatsKind) stats_kind = kRollStatsKind;
             GemmPlan p = plan_gemm_as(M, N, K, epilogue == kEpiPlain ? plain_kind : stats_kind, 1, epilogue);
-            // Where the plain GEMM takes another tile than the statistics
-            // epilogue (an LM head), both walk K in order, so that the logits
-            // stored with their statistics are the plain GEMM's bit for bit
-            // (a staggered K start gained nothing measurable here).
-            if (plain_kind != stats_kind) p.krot_on = 0;
+            // Both walk K in order, so that the logits stored with their
+            // statistics are the plain GEMM's bit for bit also where the two
+            // take different tiles (a staggered K start gained nothing
+            // measurable on the LM head).
+            if (plain_kind != stats_kind || plain_kind == kRollStatsKind) p.krot_on = 0;
             return p;
         }
         // Short N (QKV, O, down).  A CU streams its operand rows at a rate

@@ -10,8 +10,9 @@ namespace specfp8 {
 // ---- FP8 GEMM tiles ---------------------------------------------------------
 // A tile is a WM x WN grid of waves, each wave holding WTM x WTN blocks of
 // 16x16 outputs; STAGES LDS buffers rotate through the K-loop.  roll: the
-// long-prompt kernel whose operand fragments are refilled in place (one
-// fragment set; never split in K, plain epilogue only).
+// kernel whose operand fragments are refilled in place (one fragment set;
+// never split in K; plain epilogue only, but for kRollStatsKind, which also
+// has the statistics epilogue).
 struct TileShape {
     int wtm, wtn, wm, wn, stages, roll;
 };
@@ -28,13 +29,15 @@ struct TileShape {
 //  8    64 x 128  2x2 (32x64)           4        96 KiB  M <= 64 wide N; M <= 320 short N
 //  9   256 x 224  2x2 (128x112), roll   2       120 KiB  large M
 // 10   256 x 256  2x2 (128x128), roll   2       128 KiB  large M
-// 11   160 x 384  2x2 (80x192), roll    2       136 KiB  M <= 320, very wide N (LM head)
+// 11   160 x 384  2x2 (80x192), roll    2       136 KiB  M <= 320, very wide N (LM head, with statistics)
 constexpr TileShape kTiles[] = {
     {2, 2, 2, 2, 4, 0}, {5, 4, 1, 2, 4, 0}, {5, 7, 2, 2, 3, 0}, {8, 4, 2, 2, 3, 0}, {5, 6, 2, 2, 3, 0},
     {5, 4, 2, 2, 4, 0}, {5, 4, 4, 1, 3, 0}, {5, 2, 2, 2, 4, 0}, {2, 4, 2, 2, 4, 0}, {8, 7, 2, 2, 2, 1},
     {8, 8, 2, 2, 2, 1}, {5, 12, 2, 2, 2, 1},
 };
 constexpr int kTileKinds = sizeof(kTiles) / sizeof(kTiles[0]);
+// The in-place-refill tile that also has the statistics epilogue (LM head).
+constexpr int kRollStatsKind = 11;
 constexpr int tile_bm(int k) { return 16 * kTiles[k].wtm * kTiles[k].wm; }
 constexpr int tile_bn(int k) { return 16 * kTiles[k].wtn * kTiles[k].wn; }
 constexpr int tile_threads(int k) { return 64 * kTiles[k].wm * kTiles[k].wn; }

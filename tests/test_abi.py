@@ -276,6 +276,11 @@ def test_logit_stats_gemm_validation(lib):
     assert ls(lib, st=None) == NULL
     assert ls(lib, st=A16 + 4) == ALIGN
     assert ls(lib, M=0, a=None, sa=None, w=None, sw=None, y=None, st=None, ldst=G) == OK
+    # the LM head's 160 x 384 tile addresses a tile's operand rows with 32-bit
+    # offsets: 159 lda + 128 and 383 ldw + 128 must not exceed 2^32
+    lm = dict(M=320, V=128256, K=4096, ldy=128256)
+    assert ls(lib, lda=1 << 25, ldw=4096, **lm) == UNSUP
+    assert ls(lib, lda=4096, ldw=1 << 24, **lm) == UNSUP
 
 
 def accs(lib, zt=A16, ts=A16, n=4, ldn=4, zd=A16, x=A16, u=A16, B=2, k=3, V=256, T=0.7, out=A16, num=A16, ws=A16,

@@ -77,6 +77,8 @@ def _lm_operands(p, M, V, K, seed, w_std):
     (200, 1024, 4096, 0.7),         # long K: 160x128 tiles (never split here)
     (320, 6144, 1024, 0.0),         # greedy statistics
     (100, 4096, 512, 0.0),
+    (300, 32008, 256, 0.7),         # 160x384 tiles (fewer operand rows per CU than 160x224): ragged M,
+    (300, 32008, 256, 0.0),         #   a last tile of 136 columns (its second wave's column group empty)
 ])
 def test_logit_stats_vs_oracle(M, V, K, T):
     p = need_gpu()
