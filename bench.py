@@ -226,13 +226,19 @@ def vendor_gemm(torch, step, weights, reps=22):
     return res
 
 
-def lm_head_parts(torch, p, wl, reps=12):
+def lm_head_parts(torch, p, wl, reps=6):
     """The LM head of the verify pass (M = 320 rows, K = 4096 -> V = 128256)
-    followed by the stochastic acceptance, two ways: unfused (the GEMM writes
-    the logits, the acceptance reads them for its statistics) and fused (the
-    statistics come out of the GEMM epilogue and the acceptance streams only
-    the draft rows).  Seeded synthetic weights and hidden states made on the
-    device; each part timed like time_parts.  Returns mean us per part."""
+    followed by the acceptance, two ways: unfused (the GEMM writes the logits,
+    the acceptance reads them for its statistics) and fused (the statistics
+    come out of the GEMM epilogue; the stochastic acceptance then streams only
+    the draft rows, the greedy one streams nothing).  Stochastic (T = 0.7,
+    drafts sampled from the draft rows) and greedy (argmax drafts).  Seeded
+    synthetic weights and hidden states made on the device.  Each part is
+    timed as HIP-graph replays (16 calls per graph, so neither the host's
+    launch cost nor a replay's own start-up weighs on a few-microsecond
+    acceptance); the weights (525 MB)
+    are read cold every call, the logits the acceptance reads (148 MB) were
+    just written, as in the verify pass.  Returns mean us per part."""
     cfg4 = wl.CONFIGS["C4"]
     B, k, V, T = cfg4["B"], cfg4["k"], cfg4["V"], cfg4["temperature"]
     K, M = 4096, B * (cfg4["k"] + 1)
@@ -252,6 +258,8 @@ def lm_head_parts(torch, p, wl, reps=12):
     u = torch.rand((B, k + 1), generator=g, device="cuda")
     logits = torch.empty((M, V), dtype=torch.bfloat16, device="cuda")
     stats = torch.empty((M, p.logit_stats_count(M, V, K), 2), dtype=torch.float32, device="cuda")
+    stats_g = torch.empty_like(stats)
+    xg = zd.float().argmax(dim=-1).to(torch.int32)
     ws = torch.empty((p.accept_workspace_bytes(B, k, V),), dtype=torch.uint8, device="cuda")
     out = torch.empty((B, k + 1), dtype=torch.int32, device="cuda")
     num = torch.empty((B,), dtype=torch.int32, device="cuda")
@@ -262,22 +270,38 @@ def lm_head_parts(torch, p, wl, reps=12):
         "accept": lambda: p.verify_accept(zt, zd, x, u, T, workspace=ws, out_tokens=out, num_accepted=num),
         "accept_from_stats": lambda: p.verify_accept(zt, zd, x, u, T, workspace=ws, out_tokens=out,
                                                      num_accepted=num, target_stats=stats),
+        "gemm_with_argmax": lambda: p.gemm_logit_stats(a_t, sa_t, w, sw, 0.0, out=logits, stats=stats_g),
+        "accept_greedy": lambda: p.verify_accept(zt, None, xg, None, 0.0, workspace=ws, out_tokens=out,
+                                                 num_accepted=num),
+        "accept_greedy_from_stats": lambda: p.verify_accept(zt, None, xg, None, 0.0, workspace=ws, out_tokens=out,
+                                                            num_accepted=num, target_stats=stats_g),
     }
     res = {}
+    per_graph = 16
     for n, fn in parts.items():
-        evs = []
-        for _ in range(reps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn()
-            e1.record()
-            evs.append((e0, e1))
+        fn()
         torch.cuda.synchronize()
-        res[n] = round(float(np.mean([a.elapsed_time(b) for a, b in evs[2:]])) * 1e3, 1)
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for _ in range(per_graph):
+                fn()
+        gr.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            gr.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        res[n] = round(e0.elapsed_time(e1) * 1e3 / (reps * per_graph), 1)
+        del gr
     res["unfused_us"] = round(res["gemm"] + res["accept"], 1)
     res["fused_us"] = round(res["gemm_with_stats"] + res["accept_from_stats"], 1)
+    res["greedy_unfused_us"] = round(res["gemm"] + res["accept_greedy"], 1)
+    res["greedy_fused_us"] = round(res["gemm_with_argmax"] + res["accept_greedy_from_stats"], 1)
     res["gemm_tflops"] = round(2.0 * M * V * K / (res["gemm"] * 1e-6) / 1e12, 1)
-    res["workload"] = f"LM head M={M} K={K} V={V} (bf16 logits) + stochastic acceptance T={T}, k={k}"
+    res["workload"] = (f"LM head M={M} K={K} V={V} (bf16 logits) + stochastic acceptance T={T}, k={k}; "
+                       f"and + greedy acceptance (argmax drafts)")
     return res
 
 
@@ -1003,7 +1027,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--copies", type=int, default=3, help="rotated copies of weights and logits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "gemm_c3", "accept_c4", "step", "quantize_c5"],
+    ap.add_argument("--profile", choices=["traffic", "gemm_c5", "gemm_c3", "accept_c4", "step", "quantize_c5",
+                                          "lm_head"],
                     default=None,
                     help="for profiler runs: 'traffic' = a plain copy of 256 MiB (the counters' "
                          "calibration), then 3 launches of the gate|up GEMM; 'gemm_c5' = the M=4096 up and down "
@@ -1011,7 +1036,8 @@ def main(argv=None):
                          "3 rotated weight copies; 'accept_c4' = 20 stochastic and 20 greedy acceptances of the "
                          "C4 logits over 3 rotated copies; 'quantize_c5' = the M=4096 per-token and static quantize of "
                          "X [4096,4096] and H [4096,14336], cold; 'step' = --warmup and then --steps eager verify "
-                         "steps over the rotated copies, nothing else; then exit")
+                         "steps over the rotated copies, nothing else; 'lm_head' = the LM-head parts of the bench "
+                         "(plain and statistics GEMMs, stochastic and greedy acceptances) as graph replays; then exit")
     ap.add_argument("--part", choices=["gemm", "accept", "quantize"], default=None,
                     help="time one part of the step only (cold, as in the full run) and print its figures "
                          "as one JSON line")
@@ -1045,6 +1071,9 @@ def main(argv=None):
         return profile_gemm_c3(torch, p, wl)
     if args.profile == "quantize_c5":
         return profile_quantize_c5(torch, p, wl)
+    if args.profile == "lm_head":
+        log(json.dumps(lm_head_parts(torch, p, wl)))
+        return 0
     acts, weights, logits = build_inputs(torch, p, wl, args.copies)
     step = Step(torch, p, wl, acts)
     if args.profile == "step":
@@ -1130,7 +1159,10 @@ def main(argv=None):
     log(f"drafter step {more['drafter_step_us']} us; KV-cache write {more['kv_cache_write_us']} us")
     log(f"tree verification: greedy {tree['greedy_us']} us, sampling {tree['sampling_us']} us")
     log(f"LM head: gemm {lm['gemm']} us (with statistics {lm['gemm_with_stats']}); accept {lm['accept']} us "
-        f"(from statistics {lm['accept_from_stats']}); unfused {lm['unfused_us']} us, fused {lm['fused_us']} us")
+        f"(from statistics {lm['accept_from_stats']}); unfused {lm['unfused_us']} us, fused {lm['fused_us']} us; "
+        f"greedy: with argmax {lm['gemm_with_argmax']}, accept {lm['accept_greedy']} "
+        f"(from argmax {lm['accept_greedy_from_stats']}); unfused {lm['greedy_unfused_us']} us, "
+        f"fused {lm['greedy_fused_us']} us")
     gemm_us = parts["qkv"] + parts["o"] + parts["gate_up"] + parts["down"]
     gu_us, acc_us = float(np.mean(gu_step_us)), parts["accept"]
     log(f"step {ms_step * 1e3:.1f} us (eager), {ms_step_graph * 1e3:.1f} us (graph); gate_up gemm {gu_us:.1f} us; "
