@@ -242,6 +242,46 @@ __global__ __launch_bounds__(kAThreads) void greedy_partial_kernel(AcceptArgs a)
     });
 }
 
+// Entry `lane` of row r's (max logit, lowest index) statistics, or the
+// neutral (-inf, INT_MAX) past the row's entries.
+__device__ __forceinline__ float2 argmax_entry(const AcceptArgs& a, int b, int r, int lane) {
+    uint32_t nst;
+    const float2* st = row_stats(a, b, r, nst);
+    return (uint32_t)lane < nst ? st[lane] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
+}
+
+// Merged (max logit, lowest index) of row r of sequence b, for lanes of one
+// wave; `first` is the row's entry `lane` (argmax_entry), loaded beforehand.
+// The order of `better` is total, so the merge order does not matter.
+__device__ __forceinline__ int merged_argmax(const AcceptArgs& a, int b, int r, int lane, float2 first) {
+    uint32_t nst;
+    const float2* st = row_stats(a, b, r, nst);
+    float bv = first.x;
+    int bi = __float_as_int(first.y);
+    // the entries past the first 64 (many when they come from the LM-head
+    // epilogue: 668 per row at V = 128256), 16 per lane per round trip
+    for (int64_t c0 = lane + 64; c0 < nst; c0 += 16 * 64) {
+        float2 pv[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int64_t c = c0 + q * 64;
+            pv[q] = c < nst ? st[c] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
+        }
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int pi = __float_as_int(pv[q].y);
+            if (better(pv[q].x, pi, bv, bi)) { bv = pv[q].x; bi = pi; }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    return bi;
+}
+
 __global__ __launch_bounds__(1024) void greedy_final_kernel(AcceptArgs a) {
     __shared__ int g[17], s_x[16];
     const int b = blockIdx.x;
@@ -252,32 +292,7 @@ __global__ __launch_bounds__(1024) void greedy_final_kernel(AcceptArgs a) {
     // stride over the slices
     const int nw = (int)(blockDim.x >> 6);
     for (int pos = wv; pos <= a.k; pos += nw) {
-        uint32_t nst;
-        const float2* st = row_stats(a, b, pos, nst);
-        float bv = -INFINITY;
-        int bi = 0x7fffffff;
-        // loads issued 24 per lane before they are compared: a row may hold
-        // over a thousand entries when they come from the LM-head epilogue
-        // (1336 for V = 128256), which then take one round trip
-        for (int64_t c0 = lane; c0 < nst; c0 += 24 * 64) {
-            float2 pv[24];
-#pragma unroll
-            for (int q = 0; q < 24; ++q) {
-                const int64_t c = c0 + q * 64;
-                pv[q] = c < nst ? st[c] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
-            }
-#pragma unroll
-            for (int q = 0; q < 24; ++q) {
-                const int pi = __float_as_int(pv[q].y);
-                if (better(pv[q].x, pi, bv, bi)) { bv = pv[q].x; bi = pi; }
-            }
-        }
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) {
-            const float ov = __shfl_xor(bv, o, 64);
-            const int oi = __shfl_xor(bi, o, 64);
-            if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-        }
+        const int bi = merged_argmax(a, b, pos, lane, argmax_entry(a, b, pos, lane));
         if (lane == 0) g[pos] = bi;
     }
     if (t < a.k) s_x[t] = xt;
@@ -781,43 +796,6 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
 
 constexpr int kMaxTree = 64;   // nodes per sequence
 
-// Entry `lane` of row r's (max logit, lowest index) statistics, or the
-// neutral (-inf, INT_MAX) past the row's entries.
-__device__ __forceinline__ float2 argmax_entry(const AcceptArgs& a, int b, int r, int lane) {
-    uint32_t nst;
-    const float2* st = row_stats(a, b, r, nst);
-    return (uint32_t)lane < nst ? st[lane] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
-}
-
-// Merged (max logit, lowest index) of row r of sequence b, for lanes of one
-// wave; `first` is the row's entry `lane` (argmax_entry), loaded beforehand.
-// The order of `better` is total, so the merge order does not matter.
-__device__ __forceinline__ int merged_argmax(const AcceptArgs& a, int b, int r, int lane, float2 first) {
-    uint32_t nst;
-    const float2* st = row_stats(a, b, r, nst);
-    float bv = first.x;
-    int bi = __float_as_int(first.y);
-    for (int64_t c0 = lane + 64; c0 < nst; c0 += 8 * 64) {
-        float2 pv[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int64_t c = c0 + q * 64;
-            pv[q] = c < nst ? st[c] : make_float2(-INFINITY, __int_as_float(0x7fffffff));
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int pi = __float_as_int(pv[q].y);
-            if (better(pv[q].x, pi, bv, bi)) { bv = pv[q].x; bi = pi; }
-        }
-    }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const float ov = __shfl_xor(bv, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
-    return bi;
-}
 
 // Writes sequence b's outputs: the tokens of the accepted path, then the
 // emitted token, -1 padded to N+1; the path's node indices, -1 padded to N.
