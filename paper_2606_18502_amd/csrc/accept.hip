@@ -73,7 +73,6 @@ struct AcceptArgs {
     int64_t ldtst;         // row stride of tst (entries)
     uint32_t ntst;         // entries per target row in tst
     float2* tsm;           // [B][k+1] tst merged to one entry per row by the statistics kernel, or null
-    double* chunkm;        // [B][nchunk] residual mass per chunk
     double* finem;         // [B][nchunk][256] residual mass per 64-element range
     unsigned int* ctr;     // [B]
     int64_t V, nchunk;
@@ -572,6 +571,67 @@ __device__ __forceinline__ void find_owner(double v, double lo, double hi, doubl
 
 __device__ __forceinline__ void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+__device__ __forceinline__ void store_coherent(double* p, double v);
+__device__ __forceinline__ double load_coherent(const double* p);
+
+constexpr int kRunRegs = 16;   // range masses a thread keeps in registers (nchunk <= 16: V <= 262144)
+
+// The first two levels of the inverse-CDF search, by the whole last block of
+// a sequence in one round trip: its residual masses fm[0 .. nchunk * 256),
+// one per 64-element range in vocabulary order (range th of chunk ch at
+// ch * 256 + th, stored by every block of the sequence), are read in runs of
+// nchunk consecutive ranges per thread; the runs are summed in order and
+// scanned across the block, which gives the total R; the thread whose run
+// holds target = u * R walks it range by range.  Writes the chosen range
+// (index into fm) to *s_rng and the mass before it to *s_base; where rounding
+// leaves target past every interval, the last range with positive mass is
+// taken, and range 0 where there is none (R == 0 or not finite).  Returns R.
+__device__ __forceinline__ double locate_range(const double* fm, int64_t nchunk, float u, double* sh, int* s_own,
+                                               double* s_base, int* s_lastpos, int* s_rng) {
+    const int t = threadIdx.x;
+    const int64_t r0 = (int64_t)t * nchunk;
+    const bool in_regs = nchunk <= kRunRegs;
+    double v[kRunRegs];
+    double run = 0.0;
+    if (in_regs) {
+#pragma unroll
+        for (int i = 0; i < kRunRegs; ++i) v[i] = i < nchunk ? load_coherent(fm + r0 + i) : 0.0;
+#pragma unroll
+        for (int i = 0; i < kRunRegs; ++i) run += v[i];
+    } else {
+        for (int64_t i = 0; i < nchunk; ++i) run += load_coherent(fm + r0 + i);
+    }
+    double lo, hi, R;
+    block_scan_d(run, sh, lo, hi, R);
+    const double target = (double)u * R;
+    find_owner(run, lo, hi, 0.0, target, s_own, s_base, s_lastpos);
+    if (t == *s_own) {
+        double cum = *s_base, last_base = cum, pick_base = cum;
+        int64_t pick = -1, lastpos = -1;
+        auto visit = [&](int64_t i, double m) {
+            const double nx = cum + m;
+            if (m > 0.0) { lastpos = i; last_base = cum; }
+            if (pick < 0 && cum <= target && target < nx) { pick = i; pick_base = cum; }
+            cum = nx;
+        };
+        if (in_regs) {
+#pragma unroll
+            for (int i = 0; i < kRunRegs; ++i)
+                if (i < nchunk) visit(i, v[i]);
+        } else {
+            for (int64_t i = 0; i < nchunk; ++i) visit(i, load_coherent(fm + r0 + i));
+        }
+        if (pick < 0) {
+            pick = lastpos >= 0 ? lastpos : 0;
+            pick_base = lastpos >= 0 ? last_base : *s_base;
+        }
+        *s_rng = R > 0.0 ? (int)(r0 + pick) : 0;
+        *s_base = R > 0.0 ? pick_base : 0.0;
+    }
+    __syncthreads();
+    return R;
+}
+
 __device__ __forceinline__ void store_coherent(double* p, double v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -590,7 +650,7 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     __shared__ float sM[33], sZ[33];
     __shared__ double s_rm[kAThreads];
     __shared__ int s_acc[16], s_x[16];
-    __shared__ int s_j, s_last;
+    __shared__ int s_j, s_last, s_rng;
     __shared__ float s_uk;
     __shared__ double sh[kWavesPerBlock];
     __shared__ int s_own, s_lastpos;
@@ -685,7 +745,6 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
         }
     }
 
-    double* cm = a.chunkm + (int64_t)b * a.nchunk;              // chunk masses
     double* fm = a.finem + (int64_t)b * a.nchunk * kAThreads;   // range masses
     auto range_of = [&](int64_t ch, int th, int64_t& e0, int64_t& e1) {
         e0 = ch * kChunk + (int64_t)th * kPerThread;
@@ -700,17 +759,14 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
         return s_rm[t];
     };
 
-    // 3. this block's range masses and chunk total, stored device-coherently
-    //    (relaxed agent-scope atomic stores, written through the L2) and
-    //    acknowledged before the ticket is taken; the last block reads them
-    //    with device-coherent loads.  No agent-scope fence is needed (on this
-    //    chip such a fence writes back and invalidates the XCD's whole L2).
+    // 3. this block's range masses, stored device-coherently (relaxed
+    //    agent-scope atomic stores, written through the L2) and acknowledged
+    //    before the ticket is taken; the last block reads them with
+    //    device-coherent loads.  No agent-scope fence is needed (on this chip
+    //    such a fence writes back and invalidates the XCD's whole L2).
     {
         const double m = mass_of(c);
         store_coherent(fm + c * kAThreads + t, m);
-        double lo, hi, tot;
-        block_scan_d(m, sh, lo, hi, tot);
-        if (t == 0) store_coherent(cm + c, tot);
         wait_stores();
         __syncthreads();
         if (t == 0) {
@@ -721,42 +777,24 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
         if (!s_last) return;
     }
 
-    // 4. last block of sequence b.  Level 1: the chunk holding u*R.
-    double v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
-    double lo1, hi1, R;
-    block_scan_d(v1, sh, lo1, hi1, R);
+    // 4. last block of sequence b: the range of 64 elements holding u*R.
+    double R = locate_range(fm, a.nchunk, s_uk, sh, &s_own, &s_base, &s_lastpos, &s_rng);
     if (!(R > 0.0)) {
         // The residual vanished (p_j == q_j wherever it is positive): sample
-        // p_j itself.  This block recomputes every range and chunk mass.
+        // p_j itself.  This block recomputes every range mass.
         d.zd_row = nullptr;
         d.skip = -1;
-        for (int64_t ch = 0; ch < a.nchunk; ++ch) {
-            const double m = mass_of(ch);
-            store_coherent(fm + ch * kAThreads + t, m);
-            double lo, hi, tot;
-            block_scan_d(m, sh, lo, hi, tot);
-            if (t == 0) store_coherent(cm + ch, tot);
-        }
+        for (int64_t ch = 0; ch < a.nchunk; ++ch) store_coherent(fm + ch * kAThreads + t, mass_of(ch));
         wait_stores();
         __syncthreads();
-        v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
-        block_scan_d(v1, sh, lo1, hi1, R);
+        R = locate_range(fm, a.nchunk, s_uk, sh, &s_own, &s_base, &s_lastpos, &s_rng);
     }
     const double target = (double)s_uk * R;
-    find_owner(v1, lo1, hi1, 0.0, target, &s_own, &s_base, &s_lastpos);
-    const int64_t cs = s_own;
-    const double base2 = s_base;
 
-    // Level 2: the range of 64 elements within chunk cs.
-    const double v2 = load_coherent(fm + cs * kAThreads + t);
-    double lo2, hi2, tot2;
-    block_scan_d(v2, sh, lo2, hi2, tot2);
-    find_owner(v2, lo2, hi2, base2, target, &s_own, &s_base, &s_lastpos);
-
-    // Level 3: the element within the range (wave 0, one element per lane).
+    // Then the element within the range (wave 0, one element per lane).
     if (wv == 0) {
         int64_t e0, e1;
-        range_of(cs, s_own, e0, e1);
+        range_of(s_rng / kAThreads, s_rng % kAThreads, e0, e1);
         const double base3 = s_base;
         const int64_t e = e0 + lane;
         const float r = e < e1 ? (d.zd_row ? dist1<true>(d, a.c2, e) : dist1<false>(d, a.c2, e)) : 0.0f;
@@ -882,7 +920,7 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
     __shared__ int s_par[kMaxTree], s_x[kMaxTree], s_path[kMaxTree], s_kill[kMaxTree];
     __shared__ double s_p[kMaxTree];
     __shared__ float s_u[kMaxTree + 1];
-    __shared__ int s_f, s_depth, s_nkill, s_last;
+    __shared__ int s_f, s_depth, s_nkill, s_last, s_rng;
     __shared__ double sh[kWavesPerBlock];
     __shared__ int s_own, s_lastpos;
     __shared__ double s_base;
@@ -989,7 +1027,6 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
             if (off < 64) dd.kill |= 1ull << off;
         }
     };
-    double* cm = a.chunkm + (int64_t)b * a.nchunk;
     double* fm = a.finem + (int64_t)b * a.nchunk * kAThreads;
     auto range_of = [&](int64_t ch, int th, int64_t& e0, int64_t& e1) {
         e0 = ch * kChunk + (int64_t)th * kPerThread;
@@ -1004,11 +1041,7 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
         return range_mass<VEC, false>(dd, a.c2, e0, e1);
     };
     {
-        const double m = mass_of(c);
-        store_coherent(fm + c * kAThreads + t, m);
-        double lo, hi, tot;
-        block_scan_d(m, sh, lo, hi, tot);
-        if (t == 0) store_coherent(cm + c, tot);
+        store_coherent(fm + c * kAThreads + t, mass_of(c));
         wait_stores();
         __syncthreads();
         if (t == 0) {
@@ -1018,35 +1051,19 @@ __global__ __launch_bounds__(kAThreads) void tree_sample_kernel(AcceptArgs a) {
         __syncthreads();
         if (!s_last) return;
     }
-    double v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
-    double lo1, hi1, R;
-    block_scan_d(v1, sh, lo1, hi1, R);
+    double R = locate_range(fm, a.nchunk, s_u[N], sh, &s_own, &s_base, &s_lastpos, &s_rng);
     if (!(R > 0.0)) {
         // the removed tokens held all the mass: draw from P itself
         nk = 0;
-        for (int64_t ch = 0; ch < a.nchunk; ++ch) {
-            const double m = mass_of(ch);
-            store_coherent(fm + ch * kAThreads + t, m);
-            double lo, hi, tot;
-            block_scan_d(m, sh, lo, hi, tot);
-            if (t == 0) store_coherent(cm + ch, tot);
-        }
+        for (int64_t ch = 0; ch < a.nchunk; ++ch) store_coherent(fm + ch * kAThreads + t, mass_of(ch));
         wait_stores();
         __syncthreads();
-        v1 = t < a.nchunk ? load_coherent(cm + t) : 0.0;
-        block_scan_d(v1, sh, lo1, hi1, R);
+        R = locate_range(fm, a.nchunk, s_u[N], sh, &s_own, &s_base, &s_lastpos, &s_rng);
     }
     const double target = (double)s_u[N] * R;
-    find_owner(v1, lo1, hi1, 0.0, target, &s_own, &s_base, &s_lastpos);
-    const int64_t cs = s_own;
-    const double base2 = s_base;
-    const double v2 = load_coherent(fm + cs * kAThreads + t);
-    double lo2, hi2, tot2;
-    block_scan_d(v2, sh, lo2, hi2, tot2);
-    find_owner(v2, lo2, hi2, base2, target, &s_own, &s_base, &s_lastpos);
     if (wv == 0) {
         int64_t e0, e1;
-        range_of(cs, s_own, e0, e1);
+        range_of(s_rng / kAThreads, s_rng % kAThreads, e0, e1);
         const double base3 = s_base;
         Dist dd = d;
         killed_in(e0, dd);
@@ -1134,7 +1151,6 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
     char* ws = reinterpret_cast<char*>(workspace);
     a.zt = zt; a.zd = zd; a.x = x; a.u = u; a.out = out_tokens; a.num = num_accepted;
     a.stats = reinterpret_cast<float2*>(ws + p.stats_off);
-    a.chunkm = reinterpret_cast<double*>(ws + p.mass_off);
     a.finem = reinterpret_cast<double*>(ws + p.fine_off);
     a.ctr = reinterpret_cast<unsigned int*>(ws + p.ctr_off);
     a.V = V; a.nchunk = p.nchunk; a.nslice = (uint32_t)p.nschunk; a.B = (int)B; a.k = (int)k;
@@ -1190,7 +1206,6 @@ hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int
     a.zt = zt; a.zd = nullptr; a.x = x; a.u = u; a.out = out_tokens; a.num = num_accepted;
     a.parent = parent; a.nodes = accepted_nodes;
     a.stats = reinterpret_cast<float2*>(ws + p.stats_off);
-    a.chunkm = reinterpret_cast<double*>(ws + p.mass_off);
     a.finem = reinterpret_cast<double*>(ws + p.fine_off);
     a.ctr = reinterpret_cast<unsigned int*>(ws + p.ctr_off);
     a.tst = nullptr; a.ntst = 0; a.ldtst = 0;

@@ -150,8 +150,7 @@ AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {
     p.nschunk = (V + kAcceptSlice - 1) / kAcceptSlice;
     const int64_t R = 2 * k + 1;
     p.stats_off = 0;
-    p.mass_off = align256((size_t)B * R * p.nschunk * 8);     // float2 per (row, slice)
-    p.fine_off = p.mass_off + align256((size_t)B * p.nchunk * sizeof(double));
+    p.fine_off = align256((size_t)B * R * p.nschunk * 8);     // after a float2 per (row, slice)
     p.ctr_off = p.fine_off + align256((size_t)B * p.nchunk * kAcceptThreads * sizeof(double));
     p.bytes = p.ctr_off + align256((size_t)B * sizeof(unsigned int));
     if (B == 0) p.bytes = 0;
