@@ -10,10 +10,10 @@
 //   stoch_sample_kernel    (chunk, b) -> every block merges the slice statistics
 //                          of its sequence in slice order, takes the (identical)
 //                          accept/reject decisions and sums the residual
-//                          distribution over its chunk; the last block of the
-//                          sequence to finish (an atomic ticket) locates the
-//                          chunk holding u*R, scans it in vocabulary order and
-//                          writes the tokens.
+//                          distribution over its chunk's 64-element ranges;
+//                          the last block of the sequence to finish (an atomic
+//                          ticket) locates the range holding u*R, scans it in
+//                          vocabulary order and writes the tokens.
 //
 // Two variants reuse these kernels:
 //   target statistics given (the LM head's epilogue wrote them): the streaming
@@ -641,10 +641,10 @@ __device__ __forceinline__ double load_coherent(const double* p) {
 }
 
 // Sampling from the residual (or bonus) distribution of position j by inverse
-// CDF in vocabulary order, in three levels: every block stores the masses of
-// its chunk's 256 ranges of 64 elements (thread t owns range t) and the chunk
-// total; the last block of the sequence finds the chunk holding u*R, then the
-// range within it, then the element within the range (one lane each).
+// CDF in vocabulary order: every block stores the masses of its chunk's 256
+// ranges of 64 elements (thread t owns range t); the last block of the
+// sequence finds the range holding u*R (locate_range), then the element
+// within the range (one lane each).
 template <bool VEC>
 __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     __shared__ float sM[33], sZ[33];
