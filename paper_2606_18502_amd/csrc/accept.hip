@@ -571,13 +571,18 @@ __device__ __forceinline__ void find_owner(double v, double lo, double hi, doubl
 
 __device__ __forceinline__ void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-__device__ __forceinline__ void store_coherent(double* p, double v);
-__device__ __forceinline__ double load_coherent(const double* p);
+__device__ __forceinline__ void store_coherent(double* p, double v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ double load_coherent(const double* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 constexpr int kRunRegs = 16;   // range masses a thread keeps in registers (nchunk <= 16: V <= 262144)
 
-// The first two levels of the inverse-CDF search, by the whole last block of
-// a sequence in one round trip: its residual masses fm[0 .. nchunk * 256),
+// The inverse-CDF search down to one 64-element range, by the whole last
+// block of a sequence in one round trip: its residual masses fm[0 .. nchunk * 256),
 // one per 64-element range in vocabulary order (range th of chunk ch at
 // ch * 256 + th, stored by every block of the sequence), are read in runs of
 // nchunk consecutive ranges per thread; the runs are summed in order and
@@ -632,13 +637,6 @@ __device__ __forceinline__ double locate_range(const double* fm, int64_t nchunk,
     return R;
 }
 
-__device__ __forceinline__ void store_coherent(double* p, double v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ double load_coherent(const double* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // Sampling from the residual (or bonus) distribution of position j by inverse
 // CDF in vocabulary order: every block stores the masses of its chunk's 256
