@@ -1166,7 +1166,9 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
-        hipLaunchKernelGGL(greedy_final_kernel, dim3((unsigned)B), dim3(1024), 0, stream, a);
+        // one wave per position (k + 1 <= 17 positions, at most 16 waves)
+        const unsigned fw = (unsigned)(k + 1 < 16 ? k + 1 : 16);
+        hipLaunchKernelGGL(greedy_final_kernel, dim3((unsigned)B), dim3(64 * fw), 0, stream, a);
         return hipGetLastError();
     }
     a.R = (uint32_t)((k + 1) + (zd ? k : 0));
