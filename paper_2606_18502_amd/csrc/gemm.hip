@@ -898,18 +898,23 @@ __device__ __forceinline__ void roll_store_lds(const GemmArgs& g, const v4f (&ac
     const int64_t row0 = m0 + wm * kRows;
     const int col0 = n0 + wn * WTN * 16;
     // one 16-byte chunk of 8 columns: whole, or (EDGE) the columns below N.
-    // Whole chunks are stored nontemporally: the output (82 MB of logits for
-    // an LM head, 117 MB for a long prompt's up projection) would otherwise
-    // be allocated in, and written back through, the caches the operand
-    // streams use (LM head 221 -> 216 us, with statistics 225 -> 218 us; the
-    // acceptance that reads the logits next measured the same, its greedy
-    // argmax pass 1.6 us slower).
+    // Where a wave's row segments are whole 128-byte lines (256 and 384
+    // bytes: the 256x256 and 160x384 tiles), whole chunks are stored
+    // nontemporally: the output (82 MB of logits for an LM head) would
+    // otherwise be allocated in, and written back through, the caches the
+    // operand streams use (LM head 221 -> 216 us, with statistics 225 ->
+    // 218 us; the acceptance that reads the logits next measured the same,
+    // its greedy argmax pass 1.6 us slower).  The 224-byte segments of the
+    // 256x224 tile start mid-line; stored nontemporally, the lines they share
+    // were written 1.15 times, so they are stored normally.
+    constexpr bool kNontemporal = kRowBytes % 128 == 0;
     auto put = [&](int c, const u32x4& v) {
         const int64_t m = row0 + c / kChunks;
         const int n = col0 + (c % kChunks) * 8;
         uint16_t* dst = reinterpret_cast<uint16_t*>(g.y) + m * g.ldy + n;
         if (!EDGE || (m < g.M && n + 7 < g.N)) {
-            __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dst));
+            if constexpr (kNontemporal) __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dst));
+            else *reinterpret_cast<u32x4*>(dst) = v;
         } else if (m < g.M) {
             const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
             for (int e = 0; e < 8 && n + e < g.N; ++e) dst[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
