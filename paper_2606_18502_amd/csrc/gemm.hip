@@ -654,6 +654,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_fp8_kernel(GemmArgs g) {
         kstep<C, STAGES, WTM, WTN, (S) % STAGES>(g, stages, base + (S), nk, ks0, krot, m0, n0, wave, lane, wm, \
                                                  wn, acc, CUR, NXT);
     constexpr int U = (STAGES % 2 == 0) ? STAGES : 2 * STAGES;
+    static_assert(U <= 8, "the loop body below spells out at most 8 steps");
     for (int base = 0; base < nk; base += U) {
         SPEC_STEP(0, f0, f1)
         SPEC_STEP(1, f1, f0)

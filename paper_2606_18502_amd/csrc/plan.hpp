@@ -9,7 +9,8 @@ namespace specfp8 {
 
 // ---- FP8 GEMM tiles ---------------------------------------------------------
 // A tile is a WM x WN grid of waves, each wave holding WTM x WTN blocks of
-// 16x16 outputs; STAGES LDS buffers rotate through the K-loop.  roll: the
+// 16x16 outputs; STAGES LDS buffers rotate through the K-loop (deeper
+// pipelines, 6 stages of 64x128 or 8 of 64x64, measured no faster).  roll: the
 // kernel whose operand fragments are refilled in place (one fragment set;
 // never split in K; plain epilogue only, but for kRollStatsKind, which also
 // has the statistics epilogue).
