@@ -73,6 +73,9 @@ struct AcceptArgs {
     int64_t ldtst;         // row stride of tst (entries)
     uint32_t ntst;         // entries per target row in tst
     float2* tsm;           // [B][k+1] tst merged to one entry per row by the statistics kernel, or null
+    float2* zx;            // [B][k] (target, draft) logits at the draft tokens, gathered by the statistics
+                           // kernel for the sampling kernel (chain mode with a statistics pass), or null
+    uint32_t sw;           // streaming waves of the statistics grid (the first sw waves)
     double* finem;         // [B][nchunk][256] residual mass per 64-element range
     unsigned int* ctr;     // [B]
     int64_t V, nchunk;
@@ -163,16 +166,21 @@ inline unsigned stream_blocks(int64_t items, int cus) {
 }
 
 // Persistent wave loop over items it = gw, gw + GW, ...: the slice of item
-// it + GW is loaded while item it is reduced (two register buffers).
+// it + GW is loaded while item it is reduced (two register buffers).  The
+// wave id is read from the first lane, so the item, row and slice indices are
+// known to be wave-uniform and their arithmetic runs on the scalar unit
+// (C4 stochastic acceptance 46.4 -> 46.1 us).
+// Only the first a.sw waves of the grid stream (workgroups past them do side
+// work).
 template <bool VEC, class RowOf, class Body>
 __device__ __forceinline__ void stream_items(const AcceptArgs& a, RowOf row_of, Body body) {
     const int lane = threadIdx.x & (kWave - 1);
-    const uint32_t gw = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    const uint32_t GW = gridDim.x * kWavesPerBlock;
+    const uint32_t gw = blockIdx.x * kWavesPerBlock + (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const uint32_t GW = a.sw;
     auto lo = [&](uint32_t it) { return (int64_t)(it % a.nslice) * kSlice; };
     auto hi = [&](uint32_t it) { return min(lo(it) + kSlice, a.V); };
     auto clampi = [&](uint32_t it) { return it < a.items ? it : a.items - 1; };
-    if (gw >= a.items) return;
+    if (gw >= GW || gw >= a.items) return;
     Raw r0, r1;
     load_slice<VEC>(row_of(gw / a.nslice), lo(gw), hi(gw), lane, r0);
     for (uint32_t it = gw; it < a.items; it += 2 * GW) {
@@ -390,6 +398,26 @@ __global__ __launch_bounds__(kAThreads) void stoch_stats_kernel(AcceptArgs a) {
         const int r = (int)(a.rt0 + row % a.Rs);
         return (r <= a.k) ? a.zt + (b * (a.k + 1) + r) * a.V : a.zd + (b * a.k + (r - a.k - 1)) * a.V;
     };
+    // The logits at the draft tokens, which the sampling kernel's accept
+    // tests need, are gathered by the workgroups past the streaming ones (64
+    // (sequence, draft) pairs per wave), so the sampling kernel reads them in
+    // one round trip with the statistics instead of two dependent ones (the
+    // draft ids, then the logits at them).
+    const uint32_t gwave = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (a.zx && gwave >= a.sw) {
+        const uint32_t pz = (gwave - a.sw) * kWave + (uint32_t)lane;
+        if (pz < (uint32_t)a.B * (uint32_t)a.k) {
+            const int32_t xg = a.x[pz];
+            float gt = 0.0f, gd = 0.0f;
+            if (xg >= 0 && xg < a.V) {
+                const int64_t b = pz / (uint32_t)a.k, i = pz % (uint32_t)a.k;
+                gt = bf16_to_f32(a.zt[(b * (a.k + 1) + i) * a.V + xg]);
+                if (a.zd) gd = bf16_to_f32(a.zd[(b * a.k + i) * a.V + xg]);
+            }
+            a.zx[pz] = make_float2(gt, gd);
+        }
+        return;
+    }
     stream_items<VEC>(a, row_of, [&](uint32_t it, const Raw& raw) {
         const uint32_t row = it / a.nslice, c = it % a.nslice;
         const uint16_t* z = row_of(row);
@@ -662,12 +690,18 @@ __global__ __launch_bounds__(kAThreads) void stoch_sample_kernel(AcceptArgs a) {
     // The operands of the accept tests are loaded first (draft id, then the
     // two logits at it), so their round trips overlap the statistics merge;
     // so are the resampling uniform and the drafts the outputs repeat.
+    // With a statistics pass the logits at the draft tokens were gathered by
+    // it, and load with the draft ids in one round trip.
     int32_t xi = -1;
     float zx_t = 0.0f, zx_d = 0.0f, ui = 0.0f;
     if (t <= k) ui = a.u[(int64_t)b * (k + 1) + t];
     if (t < k) {
         xi = a.x[(int64_t)b * k + t];
-        if (xi >= 0 && xi < a.V) {
+        if (a.zx) {
+            const float2 g = a.zx[(int64_t)b * k + t];
+            zx_t = g.x;
+            zx_d = g.y;
+        } else if (xi >= 0 && xi < a.V) {
             zx_t = bf16_to_f32(a.zt[((int64_t)b * (k + 1) + t) * a.V + xi]);
             if (a.zd) zx_d = bf16_to_f32(a.zd[((int64_t)b * k + t) * a.V + xi]);
         }
@@ -1161,6 +1195,7 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
         a.items = (uint32_t)(B * a.Rs * p.nschunk);
         if (a.items > 0) {
             const unsigned g1 = stream_blocks(a.items, cus);
+            a.sw = g1 * kWavesPerBlock;
             if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
             else hipLaunchKernelGGL(greedy_partial_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
             hipError_t e = hipGetLastError();
@@ -1181,8 +1216,13 @@ hipError_t launch_accept(const AcceptPlan& p, const uint16_t* zt, const uint16_t
     if (tstats && a.items > 0) a.tsm = a.stats + (int64_t)B * a.Rs * p.nschunk;
     if (a.items > 0) {
         const unsigned g1 = stream_blocks(a.items, cus);
-        if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);
-        else hipLaunchKernelGGL(stoch_stats_kernel<false>, dim3(g1), dim3(kAThreads), 0, stream, a);
+        a.sw = g1 * kWavesPerBlock;
+        // workgroups past the streaming ones gather the logits at the draft
+        // tokens, 64 (sequence, draft) pairs per wave
+        a.zx = reinterpret_cast<float2*>(ws + p.zx_off);
+        const unsigned gz = (unsigned)((B * k + kAThreads - 1) / kAThreads);
+        if (vec) hipLaunchKernelGGL(stoch_stats_kernel<true>, dim3(g1 + gz), dim3(kAThreads), 0, stream, a);
+        else hipLaunchKernelGGL(stoch_stats_kernel<false>, dim3(g1 + gz), dim3(kAThreads), 0, stream, a);
     } else {
         hipLaunchKernelGGL(clear_tickets_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, stream, a.ctr,
                            (int)B);
@@ -1215,6 +1255,7 @@ hipError_t launch_accept_tree(const AcceptPlan& p, const uint16_t* zt, const int
     a.items = (uint32_t)(B * a.Rs * p.nschunk);
     const bool vec = (V % 8 == 0) && ((uintptr_t)zt % 16 == 0);
     const unsigned g1 = stream_blocks(a.items, cus);
+    a.sw = g1 * kWavesPerBlock;
     if (temperature == 0.0f) {
         a.c2 = 0.0f;
         if (vec) hipLaunchKernelGGL(greedy_partial_kernel<true>, dim3(g1), dim3(kAThreads), 0, stream, a);

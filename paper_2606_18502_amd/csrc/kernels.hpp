@@ -66,7 +66,7 @@ struct AcceptPlan {
     int64_t nchunk;        // sampling chunks per row
     int64_t schunk;        // vocabulary elements per statistics item (one wave)
     int64_t nschunk;       // statistics items per row
-    size_t stats_off, fine_off, ctr_off, bytes;
+    size_t stats_off, fine_off, ctr_off, zx_off, bytes;
 };
 AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V);
 // tstats (optional): the target rows' statistics [B*(k+1)][ld_tstats], n_tstats

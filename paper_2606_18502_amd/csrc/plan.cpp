@@ -152,7 +152,8 @@ AcceptPlan plan_accept(int64_t B, int64_t k, int64_t V) {
     p.stats_off = 0;
     p.fine_off = align256((size_t)B * R * p.nschunk * 8);     // after a float2 per (row, slice)
     p.ctr_off = p.fine_off + align256((size_t)B * p.nchunk * kAcceptThreads * sizeof(double));
-    p.bytes = p.ctr_off + align256((size_t)B * sizeof(unsigned int));
+    p.zx_off = p.ctr_off + align256((size_t)B * sizeof(unsigned int));
+    p.bytes = p.zx_off + align256((size_t)B * k * 8);                // a float2 per (sequence, draft)
     if (B == 0) p.bytes = 0;
     return p;
 }
