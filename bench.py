@@ -941,7 +941,8 @@ def profile_quantize_c5(torch, p, wl, rounds=4):
     quantize: `rounds` rounds of X [4096, 4096] and of the FFN intermediate
     [4096, 14336] (bf16 in, E4M3 codes and fp32 scales out), each rotating
     over input copies past the 256 MB Infinity Cache, then the same with a
-    static per-tensor scale.  The two shapes run different kernel instances."""
+    static per-tensor scale.  The per-token calls of the two shapes run
+    different kernel instances; the static-scale calls share one."""
     c5 = wl.CONFIGS["C5"]
     M = c5["M"]
     gen = torch.Generator(device="cuda")
