@@ -102,6 +102,27 @@ def test_stochastic_parity(B, k, V, seed, c, with_draft):
     check_chain(out, num, zt, zd, x, u, T)
 
 
+def test_stochastic_many_pairs_and_invalid_drafts():
+    """B*k = 333 (sequence, draft) pairs, past one workgroup of the statistics
+    kernel's draft-logit gather and not a multiple of its 64 per wave, with
+    draft ids out of range in both directions (each is a rejection)."""
+    p = need_gpu()
+    B, k, V, T = 37, 9, 4000, 0.7
+    say(f"stochastic B={B} k={k} V={V} invalid drafts")
+    zt, zd, x, u = _stochastic_case(B, k, V, 21, 0.97, T)
+    x[3, 0], x[10, 4], x[36, 8] = -1, V + 3, V
+    out, num = p.verify_accept(dev_bf16(zt), dev_bf16(zd), dev_i32(x), dev_f32(u), T)
+    out, num = host(out), host(num)
+    out_ref, num_ref, mg = oa.accept_stochastic(zt, zd, x, u, T, return_margins=True)
+    assert num[3] == 0 and num[10] <= 4 and num[36] <= 8
+    clear = mg > MARGIN
+    assert clear.mean() >= 0.9
+    np.testing.assert_array_equal(num[clear], num_ref[clear])
+    np.testing.assert_array_equal(out[clear], out_ref[clear])
+    _check_valid(out, num, x, V)
+    check_chain(out, num, zt, zd, x, u, T)
+
+
 def test_stochastic_full_vocab_c4():
     """C4 at full size (B=64, k=4, V=128256, T=0.7), greedy and stochastic."""
     p = need_gpu()
