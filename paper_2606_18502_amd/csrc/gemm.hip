@@ -108,6 +108,11 @@ struct GemmCfg {
     static_assert(kRows % 16 == 0, "tile rows must be multiples of 16");
     static_assert(kGroups % kWaves == 0, "every wave issues the same number of loads per stage");
     static_assert((STAGES - 1) * kGroupsPerWave < 64, "vmcnt range");
+    static constexpr int kKind = tile_kind_of(WTM, WTN, WM, WN, STAGES);
+    static_assert(kKind >= 0, "a tile of the kind table");
+    static constexpr int kReadSpan8 = kTiles[kKind].rspan8;   // schedule of a K-step (kind table)
+    static constexpr int kLoadSpan8 = kTiles[kKind].lspan8;
+    static_assert(kReadSpan8 >= 1 && kReadSpan8 <= 8 && kLoadSpan8 >= 1 && kLoadSpan8 <= 8, "spans in eighths");
 };
 
 // LDS swizzle.  gfx950's LDS has 64 banks of 4 bytes (256 bytes per cycle),
@@ -152,12 +157,11 @@ __device__ __forceinline__ void issue_stage(const GemmArgs& g, char* stage, int 
     for (int i = 0; i < C::kGroupsPerWave; ++i) issue_group<C>(g, stage, m0, n0, kbyte, wave, lane, i);
 }
 
-// Placement of the per-step work between the MFMAs of a K-step (numerators
-// over 8 of the step's MFMA count): the LDS reads of the next step are spread
-// over the first kReadSpan8/8 of the MFMAs, so they have completed by the end
-// of the step, and the stage refill loads over the first kLoadSpan8/8.
-constexpr int kReadSpan8 = 5;
-constexpr int kLoadSpan8 = 4;
+// Placement of the per-step work between the MFMAs of a K-step of the roll
+// kernel (numerator over 8 of the step's MFMA count): the stage refill loads
+// go out over the first kRollLoadSpan8/8 of the MFMAs.  (The other kernel
+// takes its spans from the kind table.)
+constexpr int kRollLoadSpan8 = 4;
 
 // vmcnt(N) with lgkmcnt/expcnt left alone (vmcnt field: bits [3:0] and [15:14]).
 template <int N>
@@ -252,8 +256,8 @@ __device__ __forceinline__ void kstep(const GemmArgs& g, char* const* stages, in
     constexpr int kMfma = WTM * WTN;
     constexpr int kReads = 2 * (WTM + WTN);
     constexpr int kG = C::kGroupsPerWave;
-    constexpr int kRSpan = (kMfma * kReadSpan8 + 7) / 8 > 0 ? (kMfma * kReadSpan8 + 7) / 8 : 1;
-    constexpr int kLSpan = (kMfma * kLoadSpan8 + 7) / 8 > 0 ? (kMfma * kLoadSpan8 + 7) / 8 : 1;
+    constexpr int kRSpan = (kMfma * C::kReadSpan8 + 7) / 8 > 0 ? (kMfma * C::kReadSpan8 + 7) / 8 : 1;
+    constexpr int kLSpan = (kMfma * C::kLoadSpan8 + 7) / 8 > 0 ? (kMfma * C::kLoadSpan8 + 7) / 8 : 1;
 #pragma unroll
     for (int t = 0; t < kMfma; ++t) {
         const int i = t / WTM, j = t % WTM;
@@ -777,7 +781,7 @@ __device__ __forceinline__ void roll_step(const uint8_t* a0, const uint8_t* w0, 
     const uint8_t* wbase = w0 + kref;
     constexpr int kMfma = WTM * WTN;
     constexpr int kG = R::kGroupsPerWave;
-    constexpr int kLSpan = (kMfma * kLoadSpan8 + 7) / 8;
+    constexpr int kLSpan = (kMfma * kRollLoadSpan8 + 7) / 8;
     // refill order: W block i after its last MFMA (i WTM + WTM - 1), A block j
     // after its last one ((WTN - 1) WTM + j), each kRollDelay MFMAs later
     auto refill = [&](auto td_c) {

@@ -13,9 +13,14 @@ namespace specfp8 {
 // pipelines, 6 stages of 64x128 or 8 of 64x64, measured no faster).  roll: the
 // kernel whose operand fragments are refilled in place (one fragment set;
 // never split in K; plain epilogue only, but for kRollStatsKind, which also
-// has the statistics epilogue).
+// has the statistics epilogue).  rspan8, lspan8: the K-step schedule of the
+// non-roll kernel, numerators over 8 of the step's MFMAs: the next step's LDS
+// operand reads go out over the first rspan8/8 of them and the stage refill
+// loads over the first lspan8/8 (chosen by cold same-run sweeps: spreading the
+// refills over the whole step took down at M = 320 from 45.8 to 42.8 us and
+// gate|up from 48.3 to 46.7 us; the short-N tiles measured best at 5/8, 4/8).
 struct TileShape {
-    int wtm, wtn, wm, wn, stages, roll;
+    int wtm, wtn, wm, wn, stages, roll, rspan8, lspan8;
 };
 
 // kind  BM x BN   waves (wave tile)     stages  LDS      used for
@@ -32,9 +37,9 @@ struct TileShape {
 // 10   256 x 256  2x2 (128x128), roll   2       128 KiB  large M
 // 11   160 x 384  2x2 (80x192), roll    2       136 KiB  M <= 320, very wide N (LM head, with statistics)
 constexpr TileShape kTiles[] = {
-    {2, 2, 2, 2, 4, 0}, {5, 4, 1, 2, 4, 0}, {5, 7, 2, 2, 3, 0}, {8, 4, 2, 2, 3, 0}, {5, 6, 2, 2, 3, 0},
-    {5, 4, 2, 2, 4, 0}, {5, 4, 4, 1, 3, 0}, {5, 2, 2, 2, 4, 0}, {2, 4, 2, 2, 4, 0}, {8, 7, 2, 2, 2, 1},
-    {8, 8, 2, 2, 2, 1}, {5, 12, 2, 2, 2, 1},
+    {2, 2, 2, 2, 4, 0, 5, 4}, {5, 4, 1, 2, 4, 0, 6, 8}, {5, 7, 2, 2, 3, 0, 6, 8}, {8, 4, 2, 2, 3, 0, 5, 4},
+    {5, 6, 2, 2, 3, 0, 5, 4}, {5, 4, 2, 2, 4, 0, 5, 4}, {5, 4, 4, 1, 3, 0, 5, 4}, {5, 2, 2, 2, 4, 0, 5, 4},
+    {2, 4, 2, 2, 4, 0, 5, 4}, {8, 7, 2, 2, 2, 1, 5, 4}, {8, 8, 2, 2, 2, 1, 5, 4}, {5, 12, 2, 2, 2, 1, 5, 4},
 };
 constexpr int kTileKinds = sizeof(kTiles) / sizeof(kTiles[0]);
 // The in-place-refill tile that also has the statistics epilogue (LM head).
@@ -42,6 +47,14 @@ constexpr int kRollStatsKind = 11;
 constexpr int tile_bm(int k) { return 16 * kTiles[k].wtm * kTiles[k].wm; }
 constexpr int tile_bn(int k) { return 16 * kTiles[k].wtn * kTiles[k].wn; }
 constexpr int tile_threads(int k) { return 64 * kTiles[k].wm * kTiles[k].wn; }
+// The non-roll kind with this wave grid and pipeline depth, or -1.
+constexpr int tile_kind_of(int wtm, int wtn, int wm, int wn, int stages) {
+    for (int k = 0; k < kTileKinds; ++k)
+        if (!kTiles[k].roll && kTiles[k].wtm == wtm && kTiles[k].wtn == wtn && kTiles[k].wm == wm &&
+            kTiles[k].wn == wn && kTiles[k].stages == stages)
+            return k;
+    return -1;
+}
 
 constexpr int kGemmBK = 128;   // bytes (= E4M3 elements) of K per step
 
