@@ -87,6 +87,8 @@ def _sample(n, count, seed):
     (700, 400, 512), (1024, 1024, 1024),                   # 256-row tile
     (1300, 672, 256), (1777, 100, 128),                    # >= 8 M-tiles: grouped tile order, ragged group
     (300, 60096, 256),                                     # 626 160x192 tiles (a wide N), ragged M
+    (250, 14336, 384), (161, 14336, 128),                  # 160x224 tiles: as many K-steps as stages, one K-step
+    (75, 12288, 384), (200, 2048, 9216),                   # 80x128 tiles: fewer K-steps than stages; K split, ragged M
 ])
 def test_gemm_parity(M, N, K):
     p = need_gpu()
